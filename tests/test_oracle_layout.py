@@ -1,0 +1,138 @@
+"""Pins for the layout oracle (CPU only): ring size, block tables, slot mapping,
+pool content after appends, window safety of the ring and storage accounting.
+
+The hand-worked cases use W = 4, PG = 2 (ring of R = 3 pages), the window size
+of the paper's prefix-tree illustration ("SWA-Aware Prefix Cache Tree"); every
+expected value below was worked out by hand from the rule stated in the test.
+"""
+
+import numpy as np
+import pytest
+
+from oracle import layout as Lo
+
+
+def test_ring_pages_closed_form():
+    assert Lo.ring_pages(128, 16) == 9          # ceil(128/16) + 1
+    assert Lo.ring_pages(128, 64) == 3
+    assert Lo.ring_pages(4, 2) == 3
+    assert Lo.ring_pages(1, 16) == 2
+    assert Lo.ring_pages(129, 64) == 4
+    with pytest.raises(ValueError):
+        Lo.ring_pages(0, 16)
+
+
+def test_block_table_hand_worked():
+    # FULL, PG = 2, final lengths 3 and 5 need 2 and 3 pages; perm handed out in order
+    perm = [4, 0, 3, 1, 2, 5]
+    t = Lo.build_block_table(Lo.FULL, None, 2, [3, 5], perm, 4)
+    assert t.tolist() == [[4, 0, -1, -1], [3, 1, 2, -1]]
+    assert t.dtype == np.int32
+    # SWA, W = 4, PG = 2: R = 3 pages per sequence whatever the length
+    t = Lo.build_block_table(Lo.SWA, 4, 2, [1, 100], [7, 6, 5, 4, 3, 2, 1, 0], 3)
+    assert t.tolist() == [[7, 6, 5], [4, 3, 2]]
+    with pytest.raises(ValueError):
+        Lo.build_block_table(Lo.FULL, None, 2, [9], list(range(10)), 4)   # needs 5 > stride 4
+
+
+def test_slot_mapping_swa_hand_worked():
+    # W = 4, PG = 2, R = 3, ring row [10, 4, 7]; 9 tokens appended at once.
+    # The ring keeps the latest R*PG = 6 positions 3..8; position j goes to
+    # ring entry (j // 2) % 3 at offset j % 2:
+    #   j=3: entry 1 -> page 4, off 1 -> slot 9     j=4: entry 2 -> page 7 -> 14
+    #   j=5: 15    j=6: entry 0 -> page 10 -> 20    j=7: 21
+    #   j=8: entry 1 -> page 4, off 0 -> slot 8     j=0,1,2: not kept (-1)
+    table = np.array([[10, 4, 7]])
+    got = Lo.slot_mapping(Lo.SWA, 4, 2, table, [0], [9])
+    assert got.tolist() == [-1, -1, -1, 9, 14, 15, 20, 21, 8]
+    # a decode step appends position 9 (length 10): entry 1 -> page 4, off 1 ->
+    # slot 9, overwriting position 3, which is outside the window [6, 9]
+    assert Lo.slot_mapping(Lo.SWA, 4, 2, table, [9], [1]).tolist() == [9]
+
+
+def test_slot_mapping_full_hand_worked():
+    table = np.array([[5, 2, -1], [0, 3, 1]])
+    # seq 0: positions 1, 2, 3 -> (5*2+1, 2*2+0, 2*2+1); seq 1: position 4 -> 1*2+0
+    got = Lo.slot_mapping(Lo.FULL, None, 2, table, [1, 4], [3, 1])
+    assert got.tolist() == [11, 4, 5, 2]
+    assert got.dtype == np.int64
+
+
+def test_apply_append_hand_worked():
+    pg, hkv, d = 2, 1, 3
+    kp = np.zeros((2, hkv, pg, d), dtype=np.uint16)
+    vp = np.zeros((2, hkv, d, pg), dtype=np.uint16)
+    kn = np.array([[[1, 2, 3]], [[4, 5, 6]], [[7, 8, 9]]], dtype=np.uint16)
+    vn = kn + 100
+    k2, v2 = Lo.apply_append(kp, vp, [3, -1, 0], kn, vn)
+    # slot 3 = page 1, offset 1; slot 0 = page 0, offset 0; token 1 dropped
+    assert k2[1, 0, 1].tolist() == [1, 2, 3] and k2[0, 0, 0].tolist() == [7, 8, 9]
+    assert v2[1, 0, :, 1].tolist() == [101, 102, 103] and v2[0, 0, :, 0].tolist() == [107, 108, 109]
+    assert int(k2.sum()) == 1 + 2 + 3 + 7 + 8 + 9
+
+
+@pytest.mark.parametrize("window,pg", [(4, 2), (128, 16), (128, 64), (1, 16), (129, 64), (5, 4)])
+def test_ring_invariants(window, pg):
+    """Across appends of random sizes: no slot written twice in one call, every
+    ring slot holds the latest position congruent to it modulo R*PG, and the
+    window of every query position stays inside the ring (window safety)."""
+    r = Lo.ring_pages(window, pg)
+    ring_len = r * pg
+    table = np.array([np.random.default_rng(0).permutation(50)[:r]])
+    held = {}
+    pos = 0
+    rng = np.random.default_rng(window * 1000 + pg)
+    for _ in range(40):
+        n = int(rng.integers(1, 3 * ring_len))
+        slots = Lo.slot_mapping(Lo.SWA, window, pg, table, [pos], [n])
+        kept = slots[slots >= 0]
+        assert len(set(kept.tolist())) == len(kept)             # one writer per slot
+        assert len(kept) == min(n, ring_len) or pos + n <= ring_len
+        for i, s in enumerate(slots):
+            if s >= 0:
+                held[int(s)] = pos + i
+        pos += n
+        # every written slot holds the latest position congruent to it
+        for s, p in held.items():
+            assert p > pos - 1 - ring_len and p <= pos - 1
+        # window safety: the query at pos-1 needs [pos-W, pos-1]; all are held
+        need = set(range(max(0, pos - window), pos))
+        assert need <= set(held.values())
+        assert Lo.ring_positions(window, pg, pos) == {
+            ((p // pg) % r, p % pg): p for p in held.values() if p >= pos - ring_len}
+
+
+def test_prefix_window_safety_for_chunks():
+    """Before a chunk at prefix P the ring holds [P - R*PG, P); the earliest key a
+    chunk query needs is P - W + 1, so reading the ring prefix is always safe."""
+    for window, pg in ((128, 64), (128, 16), (4, 2), (1, 16)):
+        r = Lo.ring_pages(window, pg)
+        for P in (1, window - 1, window, window + 1, 3 * r * pg + 5):
+            held = set(Lo.ring_positions(window, pg, P).values())
+            need = set(range(max(0, P - window + 1), P))
+            assert need <= held
+
+
+def test_storage_closed_forms():
+    hkv, d = 8, 128
+    assert Lo.page_bytes(hkv, 64, d) == 128 * 1024               # one pool page
+    assert Lo.page_bytes(1, 16, d) == 4 * 1024
+    # SWA bytes are flat in context length: NS * R * 2 pools * page bytes
+    flat = {Lo.layer_kv_bytes(Lo.SWA, 128, 64, [L] * 16, hkv, d) for L in (1, 1000, 131073, 10 ** 6)}
+    assert flat == {16 * 3 * 2 * 128 * 1024}                     # 12 MiB
+    # 70-layer stack at 16 x 131073 tokens: hybrid (10 FULL + 60 SWA) vs all FULL
+    full = Lo.layer_kv_bytes(Lo.FULL, None, 64, [131073] * 16, hkv, d)
+    assert full == 16 * 2049 * 2 * 128 * 1024                    # 8.59 GB per FULL layer
+    swa = Lo.layer_kv_bytes(Lo.SWA, 128, 64, [131073] * 16, hkv, d)
+    hybrid, all_full = 10 * full + 60 * swa, 70 * full
+    assert hybrid / all_full == pytest.approx((60 * 3 + 10 * 2049) / (70 * 2049), rel=1e-15)
+    assert 6.9 < all_full / hybrid < 7.0                         # the paper's "about 7x"
+
+
+def test_planted_ring_mistake_is_caught(monkeypatch):
+    """A ring that keeps only W positions (instead of R*PG) breaks the hand-worked
+    slot list; a ring indexed by j % R breaks it too."""
+    orig = Lo.ring_pages
+    monkeypatch.setattr(Lo, "ring_pages", lambda w, pg: orig(w, pg) - 1)
+    table = np.array([[10, 4, 7]])
+    assert Lo.slot_mapping(Lo.SWA, 4, 2, table, [0], [9]).tolist() != [-1, -1, -1, 9, 14, 15, 20, 21, 8]
