@@ -1,0 +1,206 @@
+/*
+ * hswa.h -- C ABI of libhswa: Hybrid sliding-window-attention (SWA) paged KV
+ * attention for AMD MI355X (gfx950).
+ *
+ * The method (paper: "Full-Pipeline Inference Optimization for MiMo-V2.5
+ * Series", sections "Introduction", "Compute Analysis", "KVCache Storage
+ * Analysis", "KVCache Dual-Pool Design", "SWA-Aware Prefix Cache Tree"):
+ * a model interleaves SWA layers, which attend only inside a local window of W
+ * tokens, with FULL layers, which attend to the whole context. The KV cache is
+ * split into two physical pools: a FULL pool holding every position, and an
+ * SWA pool sized for the window (a per-sequence ring of pages), so SWA storage
+ * is O(W) instead of O(L). Out-of-window SWA entries are released (here: a ring
+ * overwrite) and must never be read again.
+ *
+ * Attention computed by every call (one sequence, query at absolute position
+ * p, query head h, KV head g = h / (Hq / Hkv)):
+ *     keys j with lo(p) <= j <= p, lo(p) = 0 (FULL) or max(0, p - W + 1) (SWA)
+ *     o = sum_j softmax_j(scale * <q, k_j>) * v_j
+ * W counts the query itself (W = 1 attends only to position p).
+ *
+ * ---------------------------------------------------------------------------
+ * Conventions shared by every call
+ * ---------------------------------------------------------------------------
+ * Ownership. The caller owns every buffer. The library never allocates, frees
+ *   or keeps device memory and holds no state between calls; all calls are
+ *   thread-safe. Pointers marked "device" are device (HBM) addresses, "host"
+ *   pointers are read synchronously during the call.
+ * Streams. Compute calls enqueue on `stream` (a hipStream_t passed as void*;
+ *   NULL = the default stream) and return without synchronising. Argument
+ *   validation is synchronous and returns a status; a failed launch returns
+ *   HSWA_ERR_LAUNCH. Device-side problems surface at the caller's next
+ *   synchronisation, or at once when the environment sets HSWA_SYNC_CHECK=1.
+ *   Nothing throws across this ABI.
+ * Dtypes. q, k, v, out and the pools hold bf16 (raw 16-bit patterns). Scores,
+ *   softmax and accumulation are fp32; outputs are rounded to bf16 with
+ *   round-to-nearest-even.
+ * Layout. Per layer there is one K pool and one V pool of `num_pages` pages:
+ *     K pool: bf16 [num_pages][Hkv][page_size][head_dim]  (a row per token)
+ *     V pool: bf16 [num_pages][Hkv][head_dim][page_size]  (transposed page)
+ *   Slot s addresses page s / page_size at in-page offset s % page_size.
+ *   Every pool offset is computed in 64-bit.
+ * Block tables (int32, device, row stride `table_stride`):
+ *     FULL layer: table[b][i] = physical page of logical page i (positions
+ *                 i*PG .. i*PG+PG-1) of sequence b; needs ceil(L_b / PG)
+ *                 entries.
+ *     SWA layer:  table[b][r] = physical page of ring entry r, r < R, with
+ *                 R = hswa_ring_pages(W, PG); position j lives in ring entry
+ *                 (j / PG) mod R at offset j mod PG, so the ring holds the
+ *                 latest R*PG positions.
+ *   Entries outside [0, num_pages) are never dereferenced: keys on such pages
+ *   are treated as absent (the result is then meaningless but no memory
+ *   outside the pools is touched).
+ * Ordering. Decode: hswa_kv_append of the new token, then hswa_decode (which
+ *   reads the new token from the cache; the ring slot the new token at c
+ *   overwrites held position c - R*PG, outside the window since R*PG > W).
+ *   Prefill:
+ *   hswa_prefill first (the chunk's own keys come from k_new / v_new), then
+ *   hswa_kv_append of the chunk. For SWA this order is required: a chunk
+ *   longer than the ring overwrites prefix keys that its first queries need.
+ * Supported shapes: head_dim == 128; Hq % Hkv == 0 and 128 % (Hq/Hkv) == 0;
+ *   page_size a power of two in [16, 256]; SWA window >= 1.
+ *   Anything else returns HSWA_ERR_UNSUPPORTED or HSWA_ERR_INVALID_ARG.
+ */
+#ifndef HSWA_H
+#define HSWA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  HSWA_OK = 0,
+  HSWA_ERR_INVALID_ARG = -1, /* null pointer, negative size, inconsistent shape */
+  HSWA_ERR_UNSUPPORTED = -2, /* shape outside the supported set above          */
+  HSWA_ERR_CAPACITY = -3,    /* table stride, page count or workspace too small */
+  HSWA_ERR_LAUNCH = -4       /* the HIP runtime rejected a launch               */
+} hswa_status;
+
+/* Layer kind flag ("Compute Analysis": SWA layers attend within a local
+ * window, FULL layers attend globally). */
+typedef enum { HSWA_LAYER_FULL = 0, HSWA_LAYER_SWA = 1 } hswa_layer_kind;
+
+/* kind: hswa_layer_kind. window: W >= 1 for SWA (counts the query itself);
+ * ignored for FULL. */
+typedef struct {
+  int32_t kind;
+  int32_t window;
+} hswa_layer;
+
+/* Head geometry of one attention layer. scale multiplies <q, k>; 1/sqrt(128)
+ * is the usual choice. */
+typedef struct {
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int32_t page_size;
+  float scale;
+} hswa_shape;
+
+/* One layer's pool pair and its block table (see Layout / Block tables). */
+typedef struct {
+  void *k_pool;               /* device, bf16 [num_pages][Hkv][PG][D]          */
+  void *v_pool;               /* device, bf16 [num_pages][Hkv][D][PG]          */
+  int64_t num_pages;
+  const int32_t *block_table; /* device, int32 [ns][table_stride]              */
+  int32_t table_stride;
+} hswa_cache;
+
+/* ---- host helpers (no device access) ------------------------------------ */
+
+/* Ring pages per sequence of an SWA layer: ceil(window / page_size) + 1 (the
+ * SWA pool is sized for the window only: "KVCache Dual-Pool Design"). Returns
+ * -1 if window < 1 or page_size < 1. */
+int32_t hswa_ring_pages(int32_t window, int32_t page_size);
+
+/* Bytes of one page of one pool (K or V): Hkv * page_size * head_dim * 2.
+ * Returns -1 on a null or non-positive shape. */
+int64_t hswa_page_bytes(const hswa_shape *shape);
+
+/* Fill a block table (host memory) from a permutation of physical page ids:
+ * sequence b needs n_b pages (FULL: ceil(final_lens[b] / page_size); SWA: R)
+ * and receives perm[o_b .. o_b + n_b - 1], o_b = n_0 + ... + n_{b-1}; unused
+ * entries are -1. table_out is int32 [ns][stride]. Returns HSWA_ERR_CAPACITY
+ * if some n_b > stride or the permutation is shorter than the sum of n_b. */
+hswa_status hswa_build_block_table(hswa_layer layer, int32_t page_size, int32_t ns,
+                                   const int32_t *final_lens, const int32_t *perm,
+                                   int64_t perm_len, int32_t *table_out, int32_t stride);
+
+/* ---- device calls -------------------------------------------------------- */
+
+/* KV append with slot mapping and ring-wrap eviction ("KVCache Dual-Pool
+ * Design": the SWA pool evicts by window; "SWA-Aware Prefix Cache Tree": the
+ * release follows each chunk and each decode step).
+ *
+ * Sequence b appends the tokens cu_seqlens[b] .. cu_seqlens[b+1]-1 of k_new /
+ * v_new at positions start_pos[b], start_pos[b]+1, ...; its length afterwards
+ * is L_b = start_pos[b] + (cu_seqlens[b+1] - cu_seqlens[b]).
+ *   FULL: slot = table[b][j / PG] * PG + j % PG.
+ *   SWA:  slot = table[b][(j / PG) mod R] * PG + j % PG if j >= L_b - R*PG,
+ *         else -1 (not stored: the ring keeps the latest R*PG positions, so
+ *         overwriting the ring is the out-of-window eviction and no slot is
+ *         written twice in one call).
+ * k_new, v_new: device bf16 [total_tokens][Hkv][D]. cu_seqlens: device int32
+ * [ns+1], non-decreasing, cu_seqlens[ns] == total_tokens. start_pos: device
+ * int32 [ns]. slot_mapping_out: device int64 [total_tokens] (may be NULL).
+ * Tokens whose logical page is beyond table_stride, or whose table entry is
+ * outside [0, num_pages), are not stored and get slot -1. */
+hswa_status hswa_kv_append(hswa_layer layer, const hswa_shape *shape, const hswa_cache *cache,
+                           const void *k_new, const void *v_new, const int32_t *cu_seqlens,
+                           const int32_t *start_pos, int32_t ns, int32_t total_tokens,
+                           int64_t *slot_mapping_out, void *stream);
+
+/* Chunked prefill over a cached prefix ("Compute Analysis": chunked prefill,
+ * compute-bound; "Prefill Optimization" / "Length Bucketing Strategy": fixed
+ * chunks over prefixes of varying length).
+ *
+ * Sequence b has prefix_lens[b] = P_b cached tokens and a chunk of
+ * C_b = cu_seqlens[b+1] - cu_seqlens[b] new tokens at positions P_b .. P_b+C_b-1.
+ * Keys below P_b are read from the cache (FULL: every one; SWA: the ring,
+ * only the in-window ones), keys from P_b on are read from k_new / v_new.
+ * q: device bf16 [total_tokens][Hq][D]; k_new, v_new: device bf16
+ * [total_tokens][Hkv][D]; out: device bf16 [total_tokens][Hq][D].
+ * max_chunk_len: host, >= every C_b (sizes the grid; longer chunks are cut).
+ * Must run before the hswa_kv_append of the same chunk. */
+hswa_status hswa_prefill(hswa_layer layer, const hswa_shape *shape, const hswa_cache *cache,
+                         const void *q, const void *k_new, const void *v_new,
+                         const int32_t *cu_seqlens, const int32_t *prefix_lens, int32_t ns,
+                         int32_t total_tokens, int32_t max_chunk_len, void *out, void *stream);
+
+/* Workspace bytes hswa_decode needs for a FULL layer (0 for an SWA layer is
+ * enough): fp32 partial outputs and log-sum-exps of every split-KV piece.
+ * Returns 0 on an invalid shape. */
+size_t hswa_decode_workspace_bytes(const hswa_shape *shape, int32_t ns, int32_t max_context_len);
+
+/* Keys per split-KV piece that hswa_decode uses for a FULL layer; pieces are
+ * [s*len, (s+1)*len) in logical positions, so results do not depend on where
+ * pages sit physically. Returns -1 on an invalid shape. */
+int32_t hswa_decode_split_len(const hswa_shape *shape, int32_t ns, int32_t max_context_len);
+
+/* Decode: one query per sequence at position c_b = context_lens[b] - 1, where
+ * context_lens counts the cached tokens including the one just appended
+ * ("KVCache Storage Analysis": decode is memory-bound). SWA layers read at most
+ * W keys from the ring in a single pass; FULL layers split the context into
+ * pieces of hswa_decode_split_len keys, write fp32 partials to the workspace
+ * and merge them by log-sum-exp.
+ * q: device bf16 [ns][Hq][D]; context_lens: device int32 [ns], each in
+ * [1, max_context_len] (values above max_context_len are clamped to it, values
+ * below 1 give a zero output row); out: device bf16 [ns][Hq][D];
+ * workspace: device, >= hswa_decode_workspace_bytes (FULL only; may be NULL
+ * for SWA). */
+hswa_status hswa_decode(hswa_layer layer, const hswa_shape *shape, const hswa_cache *cache,
+                        const void *q, const int32_t *context_lens, int32_t ns,
+                        int32_t max_context_len, void *workspace, size_t workspace_bytes,
+                        void *out, void *stream);
+
+/* Static string naming a status. */
+const char *hswa_status_string(hswa_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HSWA_H */

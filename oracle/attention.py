@@ -90,6 +90,8 @@ def masked_attention(q, k, v, q_pos, window, scale=None) -> np.ndarray:
     if scale is None:
         scale = default_scale(d)
     group = hq // hkv
+    if tq == 0:
+        return np.zeros((0, hq, d), dtype=np.float64)
 
     mask = allowed_mask(q_pos, num_keys, window)          # [Tq, L]
     out = np.zeros((tq, hq, d), dtype=np.float64)

@@ -1,0 +1,65 @@
+// Internal launcher interface between the C ABI layer (api.hip) and the
+// kernels. Arguments are validated by the caller before these are reached.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hswa {
+
+constexpr int kHeadDim = 128;  // the only head dim the kernels are built for
+
+// Pool geometry and block table of one layer, as the kernels see it.
+struct PoolView {
+  uint16_t *k_pool;       // bf16 [num_pages][Hkv][PG][D]
+  uint16_t *v_pool;       // bf16 [num_pages][Hkv][D][PG]
+  int64_t num_pages;
+  const int32_t *table;   // int32 [ns][stride]
+  int32_t stride;
+  int32_t pg_shift;       // log2(page size)
+  int32_t ring;           // ring pages R (SWA) or 0 (FULL)
+  int32_t window;         // SWA window W, or 0 for FULL
+};
+
+struct AppendParams {
+  PoolView pool;
+  const uint16_t *k_new;  // [T][Hkv][D]
+  const uint16_t *v_new;  // [T][Hkv][D]
+  const int32_t *cu_seqlens;
+  const int32_t *start_pos;
+  int64_t *slot_out;      // [T] or null
+  int32_t ns, total_tokens, hkv;
+};
+
+struct DecodeParams {
+  PoolView pool;
+  const uint16_t *q;      // [ns][Hq][D]
+  const int32_t *ctx_lens;
+  uint16_t *out;          // [ns][Hq][D]
+  float *ws_o;            // FULL split partials [ns][Hq][max_splits][D]
+  float *ws_lse;          // [ns][Hq][max_splits]
+  int32_t ns, hq, hkv, group, max_ctx;
+  int32_t split_len, max_splits;  // max_splits == 1 => single pass, no workspace
+  float scale_log2;       // scale * log2(e)
+};
+
+struct PrefillParams {
+  PoolView pool;
+  const uint16_t *q;      // [T][Hq][D]
+  const uint16_t *k_new;  // [T][Hkv][D]
+  const uint16_t *v_new;  // [T][Hkv][D]
+  const int32_t *cu_seqlens;
+  const int32_t *prefix_lens;
+  uint16_t *out;          // [T][Hq][D]
+  int32_t ns, total_tokens, max_chunk_len, hq, hkv, group;
+  float scale_log2;
+};
+
+hipError_t launch_kv_append(const AppendParams &p, hipStream_t stream);
+hipError_t launch_decode(const DecodeParams &p, hipStream_t stream);
+hipError_t launch_prefill(const PrefillParams &p, hipStream_t stream);
+
+// Split-KV piece length (keys) for a FULL decode; a multiple of 256.
+int32_t decode_split_len(int32_t ns, int32_t hkv, int32_t group, int32_t max_ctx);
+
+}  // namespace hswa

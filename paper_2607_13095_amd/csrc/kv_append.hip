@@ -1,0 +1,124 @@
+// KV append: slot mapping and scatter of new K/V rows into the paged pools.
+//
+// Dual-pool layout ("KVCache Dual-Pool Design"): a FULL layer keeps every
+// position; an SWA layer keeps a ring of R = ceil(W/PG)+1 pages per sequence,
+// and the ring overwrite is the out-of-window eviction that follows every chunk
+// and every decode step ("SWA-Aware Prefix Cache Tree").
+//
+// One workgroup handles 8 consecutive tokens of the flattened batch. The K row
+// of a token is one contiguous 256-byte run per KV head in the pool; V pages
+// are stored transposed ([D][PG] per head), so 8 tokens that land on 8
+// consecutive, 8-aligned slots of one page are written as one 16-byte store
+// per (head, dim); anything else falls back to 2-byte stores.
+#include "hswa_common.h"
+#include "hswa_launch.h"
+
+namespace hswa {
+namespace {
+
+constexpr int kTokPerBlock = 8;
+constexpr int kThreads = 256;
+
+// Sequence of flattened token t: the b with cu[b] <= t < cu[b+1] (-1 if none).
+__device__ int find_seq(const int32_t *cu, int ns, int t) {
+  int lo = 0, hi = ns;  // answer in [0, ns)
+  if (ns <= 0 || t < cu[0] || t >= cu[ns]) return -1;
+  while (hi - lo > 1) {
+    int mid = (lo + hi) >> 1;
+    if (cu[mid] <= t) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
+__device__ int64_t slot_of_token(const AppendParams &p, int t) {
+  const int b = find_seq(p.cu_seqlens, p.ns, t);
+  if (b < 0) return -1;
+  const int64_t start = p.start_pos[b];
+  const int64_t j = start + (t - p.cu_seqlens[b]);
+  const int64_t len_after = start + (p.cu_seqlens[b + 1] - p.cu_seqlens[b]);
+  if (j < 0) return -1;
+  const PoolView &pv = p.pool;
+  const int64_t pg = int64_t(1) << pv.pg_shift;
+  int64_t lp = j >> pv.pg_shift;
+  if (pv.ring > 0) {
+    if (j < len_after - pv.ring * pg) return -1;  // the ring keeps the latest R*PG
+    lp = lp % pv.ring;
+  }
+  if (lp >= pv.stride) return -1;
+  const int64_t page = pv.table[int64_t(b) * pv.stride + lp];
+  if (page < 0 || page >= pv.num_pages) return -1;
+  return page * pg + (j & (pg - 1));
+}
+
+__global__ __launch_bounds__(kThreads) void kv_append_kernel(AppendParams p) {
+  __shared__ int64_t s_slot[kTokPerBlock];
+  const int t0 = blockIdx.x * kTokPerBlock;
+  const int tid = threadIdx.x;
+  const int ntok = min(kTokPerBlock, p.total_tokens - t0);
+  if (tid < ntok) {
+    const int64_t s = slot_of_token(p, t0 + tid);
+    s_slot[tid] = s;
+    if (p.slot_out) p.slot_out[t0 + tid] = s;
+  }
+  __syncthreads();
+
+  const PoolView &pv = p.pool;
+  const int pg = 1 << pv.pg_shift;
+  const int hkv = p.hkv;
+  const int row16 = kHeadDim / 8;  // 16-byte pieces per K row
+
+  // K rows: contiguous per (page, head, offset).
+  for (int i = tid; i < ntok * hkv * row16; i += kThreads) {
+    const int tok = i / (hkv * row16);
+    const int rem = i - tok * hkv * row16;
+    const int g = rem / row16, c = rem - g * row16;
+    const int64_t s = s_slot[tok];
+    if (s < 0) continue;
+    const int64_t page = s >> pv.pg_shift, off = s & (pg - 1);
+    const u32x4 v = ldg128(p.k_new + ((int64_t)(t0 + tok) * hkv + g) * kHeadDim + c * 8);
+    stg128(pv.k_pool + ((page * hkv + g) * pg + off) * kHeadDim + c * 8, v);
+  }
+
+  // V: transposed pages.
+  bool run = ntok == kTokPerBlock && s_slot[0] >= 0 && (s_slot[0] & 7) == 0;
+#pragma unroll
+  for (int i = 1; i < kTokPerBlock; ++i) run = run && s_slot[i] == s_slot[0] + i;
+  const int nvec = hkv * kHeadDim;
+  if (run) {
+    const int64_t page = s_slot[0] >> pv.pg_shift, off = s_slot[0] & (pg - 1);
+    for (int e = tid; e < nvec; e += kThreads) {
+      const int g = e / kHeadDim, d = e - g * kHeadDim;
+      const uint16_t *src = p.v_new + ((int64_t)t0 * hkv + g) * kHeadDim + d;
+      u32x4 w;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const uint32_t lo = src[(int64_t)(2 * k) * hkv * kHeadDim];
+        const uint32_t hi = src[(int64_t)(2 * k + 1) * hkv * kHeadDim];
+        w[k] = lo | (hi << 16);
+      }
+      stg128(pv.v_pool + ((page * hkv + g) * kHeadDim + d) * pg + off, w);
+    }
+  } else {
+    for (int i = tid; i < ntok * nvec; i += kThreads) {
+      const int tok = i / nvec;
+      const int e = i - tok * nvec;
+      const int g = e / kHeadDim, d = e - g * kHeadDim;
+      const int64_t s = s_slot[tok];
+      if (s < 0) continue;
+      const int64_t page = s >> pv.pg_shift, off = s & (pg - 1);
+      pv.v_pool[((page * hkv + g) * kHeadDim + d) * pg + off] =
+          p.v_new[((int64_t)(t0 + tok) * hkv + g) * kHeadDim + d];
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_kv_append(const AppendParams &p, hipStream_t stream) {
+  if (p.total_tokens <= 0) return hipSuccess;
+  const int blocks = (p.total_tokens + kTokPerBlock - 1) / kTokPerBlock;
+  hipLaunchKernelGGL(kv_append_kernel, dim3(blocks), dim3(kThreads), 0, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace hswa

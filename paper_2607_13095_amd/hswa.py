@@ -1,0 +1,270 @@
+"""Python binding of libhswa (ctypes): argument marshalling only.
+
+Every call checks device, dtype, contiguity and sizes of the torch tensors it
+is given, passes their device pointers and the current HIP stream to the C ABI
+(``include/hswa.h``) and raises ``HswaError`` on a non-OK status. All compute
+runs in the library's HIP kernels; there is no fallback of any kind: if
+``libhswa.so`` is not built, ``load()`` raises.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libhswa.so")
+
+HSWA_LAYER_FULL = 0
+HSWA_LAYER_SWA = 1
+
+STATUS = {0: "HSWA_OK", -1: "HSWA_ERR_INVALID_ARG", -2: "HSWA_ERR_UNSUPPORTED", -3: "HSWA_ERR_CAPACITY",
+          -4: "HSWA_ERR_LAUNCH"}
+
+EXPORTS = ["hswa_ring_pages", "hswa_page_bytes", "hswa_build_block_table", "hswa_kv_append", "hswa_prefill",
+           "hswa_decode_workspace_bytes", "hswa_decode_split_len", "hswa_decode", "hswa_status_string"]
+
+
+class HswaError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {STATUS.get(status, status)}")
+        self.status = status
+
+
+class _Layer(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("window", ctypes.c_int32)]
+
+
+class _Shape(ctypes.Structure):
+    _fields_ = [("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("page_size", ctypes.c_int32), ("scale", ctypes.c_float)]
+
+
+class _Cache(ctypes.Structure):
+    _fields_ = [("k_pool", ctypes.c_void_p), ("v_pool", ctypes.c_void_p), ("num_pages", ctypes.c_int64),
+                ("block_table", ctypes.c_void_p), ("table_stride", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def load():
+    """Load libhswa.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2607_13095_amd.build_lib`")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    LP, SP, CP = _Layer, ctypes.POINTER(_Shape), ctypes.POINTER(_Cache)
+    sig = {
+        "hswa_ring_pages": (I32, [I32, I32]),
+        "hswa_page_bytes": (I64, [SP]),
+        "hswa_build_block_table": (ctypes.c_int, [LP, I32, I32, P, P, I64, P, I32]),
+        "hswa_kv_append": (ctypes.c_int, [LP, SP, CP, P, P, P, P, I32, I32, P, P]),
+        "hswa_prefill": (ctypes.c_int, [LP, SP, CP, P, P, P, P, P, I32, I32, I32, P, P]),
+        "hswa_decode_workspace_bytes": (SZ, [SP, I32, I32]),
+        "hswa_decode_split_len": (I32, [SP, I32, I32]),
+        "hswa_decode": (ctypes.c_int, [LP, SP, CP, P, P, I32, I32, P, SZ, P, P]),
+        "hswa_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype, fn.argtypes = res, args
+    _lib = lib
+    return lib
+
+
+# ---------------------------------------------------------------------------
+# argument objects
+# ---------------------------------------------------------------------------
+
+class Layer:
+    """Layer-kind flag {SWA(W), FULL}."""
+
+    def __init__(self, kind: str, window: int = 0):
+        if kind not in ("full", "swa"):
+            raise ValueError(kind)
+        self.kind, self.window = kind, int(window)
+
+    @classmethod
+    def full(cls):
+        return cls("full")
+
+    @classmethod
+    def swa(cls, window: int):
+        return cls("swa", window)
+
+    def c(self):
+        return _Layer(HSWA_LAYER_SWA if self.kind == "swa" else HSWA_LAYER_FULL, self.window)
+
+
+class Shape:
+    def __init__(self, num_q_heads, num_kv_heads, head_dim=128, page_size=64, scale=None):
+        self.num_q_heads, self.num_kv_heads = int(num_q_heads), int(num_kv_heads)
+        self.head_dim, self.page_size = int(head_dim), int(page_size)
+        self.scale = float(1.0 / np.sqrt(head_dim) if scale is None else scale)
+
+    def c(self):
+        return _Shape(self.num_q_heads, self.num_kv_heads, self.head_dim, self.page_size, self.scale)
+
+
+def _ptr(t, name, dtypes, numel=None):
+    import torch
+
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must live on the GPU")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name}: dtype {t.dtype} not in {dtypes}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if numel is not None and t.numel() < numel:
+        raise ValueError(f"{name} has {t.numel()} elements, needs {numel}")
+    return t.data_ptr()
+
+
+def _bf16():
+    import torch
+
+    return (torch.bfloat16,)
+
+
+def _i32():
+    import torch
+
+    return (torch.int32,)
+
+
+class Cache:
+    """One layer's K pool, V pool and block table (device tensors).
+
+    k_pool: bf16 [num_pages, Hkv, PG, D]; v_pool: bf16 [num_pages, Hkv, D, PG];
+    block_table: int32 [ns, stride].
+    """
+
+    def __init__(self, k_pool, v_pool, block_table):
+        if k_pool.dim() != 4 or v_pool.dim() != 4 or block_table.dim() != 2:
+            raise ValueError("pools are 4-D, the block table is 2-D")
+        npg, hkv, pg, d = k_pool.shape
+        if tuple(v_pool.shape) != (npg, hkv, d, pg):
+            raise ValueError("v_pool must be [num_pages, Hkv, D, PG]")
+        self.k_pool, self.v_pool, self.block_table = k_pool, v_pool, block_table
+        self.num_pages, self.stride = int(npg), int(block_table.shape[1])
+
+    def c(self):
+        return _Cache(_ptr(self.k_pool, "k_pool", _bf16()), _ptr(self.v_pool, "v_pool", _bf16()), self.num_pages,
+                      _ptr(self.block_table, "block_table", _i32()), self.stride)
+
+
+def _stream(stream):
+    import torch
+
+    if stream is None:
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, int):
+        return ctypes.c_void_p(stream)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _check(status, where):
+    if status != 0:
+        raise HswaError(status, where)
+
+
+# ---------------------------------------------------------------------------
+# host helpers
+# ---------------------------------------------------------------------------
+
+def ring_pages(window: int, page_size: int) -> int:
+    return int(load().hswa_ring_pages(int(window), int(page_size)))
+
+
+def page_bytes(shape: Shape) -> int:
+    sh = shape.c()
+    return int(load().hswa_page_bytes(ctypes.byref(sh)))
+
+
+def build_block_table(layer: Layer, page_size: int, final_lens: Sequence[int], perm, stride: int) -> np.ndarray:
+    """Host block table int32 [ns, stride] from a page permutation."""
+    lens = np.ascontiguousarray(np.asarray(final_lens, dtype=np.int32))
+    perm = np.ascontiguousarray(np.asarray(perm, dtype=np.int32))
+    out = np.empty((lens.size, int(stride)), dtype=np.int32)
+    st = load().hswa_build_block_table(layer.c(), int(page_size), int(lens.size), lens.ctypes.data,
+                                       perm.ctypes.data if perm.size else None, int(perm.size), out.ctypes.data,
+                                       int(stride))
+    _check(st, "hswa_build_block_table")
+    return out
+
+
+def decode_workspace_bytes(shape: Shape, ns: int, max_context_len: int) -> int:
+    sh = shape.c()
+    return int(load().hswa_decode_workspace_bytes(ctypes.byref(sh), int(ns), int(max_context_len)))
+
+
+def decode_split_len(shape: Shape, ns: int, max_context_len: int) -> int:
+    sh = shape.c()
+    return int(load().hswa_decode_split_len(ctypes.byref(sh), int(ns), int(max_context_len)))
+
+
+# ---------------------------------------------------------------------------
+# device calls
+# ---------------------------------------------------------------------------
+
+def kv_append(layer: Layer, shape: Shape, cache: Cache, k_new, v_new, cu_seqlens, start_pos,
+              slot_mapping_out=None, stream=None):
+    """Append k_new / v_new [T, Hkv, D] (bf16) to the pools; see hswa_kv_append."""
+    import torch
+
+    ns = int(cu_seqlens.numel()) - 1
+    t = int(k_new.shape[0]) if k_new.dim() else 0
+    row = shape.num_kv_heads * shape.head_dim
+    args = (_ptr(k_new, "k_new", _bf16(), t * row), _ptr(v_new, "v_new", _bf16(), t * row),
+            _ptr(cu_seqlens, "cu_seqlens", _i32(), ns + 1), _ptr(start_pos, "start_pos", _i32(), ns))
+    slots = _ptr(slot_mapping_out, "slot_mapping_out", (torch.int64,), t) if slot_mapping_out is not None else None
+    sh, ca = shape.c(), cache.c()
+    st = load().hswa_kv_append(layer.c(), ctypes.byref(sh), ctypes.byref(ca), *args, ns, t, slots, _stream(stream))
+    _check(st, "hswa_kv_append")
+
+
+def prefill(layer: Layer, shape: Shape, cache: Cache, q, k_new, v_new, cu_seqlens, prefix_lens,
+            max_chunk_len: int, out, stream=None):
+    """Chunked prefill; q, out [T, Hq, D], k_new / v_new [T, Hkv, D]; see hswa_prefill."""
+    ns = int(cu_seqlens.numel()) - 1
+    t = int(q.shape[0])
+    qrow, krow = shape.num_q_heads * shape.head_dim, shape.num_kv_heads * shape.head_dim
+    args = (_ptr(q, "q", _bf16(), t * qrow), _ptr(k_new, "k_new", _bf16(), t * krow),
+            _ptr(v_new, "v_new", _bf16(), t * krow), _ptr(cu_seqlens, "cu_seqlens", _i32(), ns + 1),
+            _ptr(prefix_lens, "prefix_lens", _i32(), ns))
+    o = _ptr(out, "out", _bf16(), t * qrow)
+    sh, ca = shape.c(), cache.c()
+    st = load().hswa_prefill(layer.c(), ctypes.byref(sh), ctypes.byref(ca), *args, ns, t, int(max_chunk_len), o,
+                             _stream(stream))
+    _check(st, "hswa_prefill")
+
+
+def decode(layer: Layer, shape: Shape, cache: Cache, q, context_lens, max_context_len: int, out,
+           workspace=None, stream=None):
+    """Decode one query per sequence; q, out [NS, Hq, D]; see hswa_decode."""
+    import torch
+
+    ns = int(context_lens.numel())
+    qrow = shape.num_q_heads * shape.head_dim
+    qp = _ptr(q, "q", _bf16(), ns * qrow)
+    cp = _ptr(context_lens, "context_lens", _i32(), ns)
+    o = _ptr(out, "out", _bf16(), ns * qrow)
+    wp, wbytes = None, 0
+    if workspace is not None:
+        wp = _ptr(workspace, "workspace", (torch.uint8, torch.float32, torch.int32))
+        wbytes = workspace.numel() * workspace.element_size()
+    sh, ca = shape.c(), cache.c()
+    st = load().hswa_decode(layer.c(), ctypes.byref(sh), ctypes.byref(ca), qp, cp, ns, int(max_context_len), wp,
+                            wbytes, o, _stream(stream))
+    _check(st, "hswa_decode")

@@ -1,0 +1,99 @@
+"""GPU parity of hswa_decode against the fp64 oracle over the contiguous
+history: SWA single pass over the ring, FULL split-KV with log-sum-exp merge,
+edge positions around page, window, ring and split boundaries, GQA groups
+from 1 to 32, and page sizes 16 and 64."""
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import attention as OA
+from paper_2607_13095_amd import hswa
+from tests.hswa_testlib import (SeqHistory, append_history, assert_close, i32, make_layer, to_dev, to_f64)
+
+pytestmark = pytest.mark.gpu
+
+
+def run_decode(kind, window, pg, hq, hkv, ctxs, seed, fill=float("nan"), perm_seed=None):
+    """Cache c_b tokens, append the token at c_b, decode it; returns (gpu, ref)."""
+    ns = len(ctxs)
+    final = [c + 1 for c in ctxs]
+    shape = hswa.Shape(hq, hkv, 128, pg)
+    layer, kv = make_layer(kind, window, shape, final, perm_seed or seed, fill=fill)
+    hist = SeqHistory(final, hkv, 128, *seed)
+    append_history(layer, shape, kv, hist, [0] * ns, ctxs)
+    append_history(layer, shape, kv, hist, ctxs, final)
+    qbits = synth.normal_bf16((ns, hq, 128), *seed, synth.TAG_QDEC)
+    out = torch.empty((ns, hq, 128), dtype=torch.bfloat16, device="cuda")
+    maxc = max(final)
+    wsb = hswa.decode_workspace_bytes(shape, ns, maxc)
+    ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device="cuda") if kind == "full" else None
+    hswa.decode(layer, shape, kv.cache, to_dev(qbits), i32(final), maxc, out, workspace=ws)
+    torch.cuda.synchronize()
+    gpu = to_f64(out)
+    qf = OA.bf16_bits_to_f64(qbits)
+    w = window if kind == "swa" else None
+    ref = np.stack([OA.decode(qf[b], OA.bf16_bits_to_f64(hist.k[b]), OA.bf16_bits_to_f64(hist.v[b]), w)
+                    for b in range(ns)])
+    return gpu, ref
+
+
+SWA_CTX = [0, 1, 15, 16, 17, 63, 64, 65, 126, 127, 128, 129, 143, 144, 145, 191, 192, 193, 1000, 4097]
+
+
+@pytest.mark.parametrize("pg", [16, 64])
+@pytest.mark.parametrize("window", [1, 2, 127, 128, 129])
+def test_decode_swa_edges(gpu_lib, pg, window):
+    print(f"[decode-swa] pg={pg} W={window}", flush=True)
+    gpu, ref = run_decode("swa", window, pg, 64, 8, SWA_CTX, (200, pg, window))
+    assert_close(gpu, ref, f"swa W={window} PG={pg}")
+
+
+@pytest.mark.parametrize("hq,hkv", [(8, 8), (8, 1), (16, 1), (32, 1), (64, 8)])
+def test_decode_groups(gpu_lib, hq, hkv):
+    print(f"[decode-groups] hq={hq} hkv={hkv}", flush=True)
+    ctxs = [5, 200, 777, 2048, 3000]
+    for kind, window in (("swa", 128), ("full", 0)):
+        gpu, ref = run_decode(kind, window, 64, hq, hkv, ctxs, (201, hq, hkv))
+        assert_close(gpu, ref, f"{kind} hq={hq} hkv={hkv}")
+
+
+def test_decode_window_one_is_exact_value(gpu_lib):
+    """W = 1: the output is V at the query's own position, bit for bit."""
+    ctxs = [0, 3, 64, 191, 192, 500]
+    shape_hq, shape_hkv = 16, 2
+    gpu, ref = run_decode("swa", 1, 16, shape_hq, shape_hkv, ctxs, (202,))
+    assert np.array_equal(gpu, ref)
+
+
+@pytest.mark.parametrize("pg", [16, 64])
+def test_decode_full_split_boundaries(gpu_lib, pg):
+    shape = hswa.Shape(64, 8, 128, pg)
+    ns = 6
+    maxc = 5000
+    sl = hswa.decode_split_len(shape, ns, maxc)
+    assert sl % 256 == 0 and sl > 0
+    # contexts (keys incl. the new token) at split multiples +-1, and the max
+    ctxs = [sl - 2, sl - 1, sl, 2 * sl - 1, 2 * sl, maxc - 1]
+    assert max(c + 1 for c in ctxs) == maxc
+    print(f"[decode-full-split] pg={pg} split_len={sl}", flush=True)
+    gpu, ref = run_decode("full", 0, pg, 64, 8, ctxs, (203, pg))
+    assert_close(gpu, ref, f"full split PG={pg}")
+
+
+def test_decode_full_long(gpu_lib):
+    ctxs = [1, 100, 32767, 20000, 8191]
+    gpu, ref = run_decode("full", 0, 64, 64, 8, ctxs, (204,))
+    assert_close(gpu, ref, "full long")
+
+
+def test_decode_context_clamp_and_empty(gpu_lib):
+    """context_lens < 1 give zero rows; ns = 0 is a no-op."""
+    shape = hswa.Shape(8, 1, 128, 16)
+    layer, kv = make_layer("full", 0, shape, [64], (205,))
+    q = torch.zeros((2, 8, 128), dtype=torch.bfloat16, device="cuda")
+    out = torch.full((2, 8, 128), 7.0, dtype=torch.bfloat16, device="cuda")
+    hswa.decode(layer, shape, kv.cache, q, i32([0, -3]), 64, out)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(out).item() == 0
