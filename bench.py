@@ -1,0 +1,365 @@
+"""Benchmark of the hybrid-SWA paged attention hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--no-prefill]
+
+Workload (the decode configuration the headline metric is quoted on):
+  64 sequences, cached contexts uniform in [1024, 32768], one SWA layer
+  (W = 128) and one FULL layer, 64 query / 8 KV heads, head dim 128, bf16,
+  page size 64, pages placed by a seeded permutation. One step appends one new
+  token per sequence to both layers (hswa_kv_append) and decodes it
+  (hswa_decode): the whole decode hot path. Inputs are resident in HBM before
+  the timed region.
+
+Also measured (same run, reported under "prefill"): chunked prefill of 4
+sequences with an 8192-token cached prefix and a 2048-token chunk, one SWA and
+one FULL layer (hswa_prefill then hswa_kv_append).
+
+value = algorithmic decode bytes (K and V of every visible key read once per
+(sequence, KV head, layer), plus q and o) / step time. The roofline entry is
+for the FULL-layer decode call (split-KV kernel + log-sum-exp merge), timed with
+HIP events on the stream it runs on, inside the timed region.
+The CPU baseline is the fp64 oracle on a bounded sample of the same workload.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2516.6
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-prefill", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target oracle time for the CPU baseline")
+    return ap.parse_args()
+
+
+# ----------------------------------------------------------------------------
+# decode workload
+# ----------------------------------------------------------------------------
+
+class DecodeBench:
+    def __init__(self, wl):
+        import torch
+
+        import synth
+        from paper_2607_13095_amd import hswa
+        from paper_2607_13095_amd.kvcache import LayerKV, pages_for
+
+        self.wl = wl
+        dev = "cuda"
+        hq, hkv, d, pg, W = wl.hq, wl.hkv, wl.head_dim, wl.page_size, wl.window
+        ns = wl.ns
+        self.ctx = np.asarray(wl.prefix, dtype=np.int64)          # cached tokens c_b
+        self.final = (self.ctx + 1).tolist()                       # context incl. the new token
+        self.shape = hswa.Shape(hq, hkv, d, pg)
+        self.maxc = int(max(self.final))
+        i32 = lambda x: torch.as_tensor(np.asarray(x, dtype=np.int32), device=dev)  # noqa: E731
+        self.layers = []
+        for li, kind in enumerate(wl.layers):
+            layer = hswa.Layer.swa(W) if kind == "swa" else hswa.Layer.full()
+            npages = pages_for(layer, pg, self.final)
+            kv = LayerKV(layer, self.shape, self.final, perm=synth.page_permutation(npages, wl.seed, li))
+            # history: positions [0, c_b] of every sequence, drawn on the GPU
+            T = int(self.ctx.sum())
+            k_hist = synth.torch_normal_bf16((T, hkv, d), dev, wl.seed, li, 0, synth.TAG_K)
+            v_hist = synth.torch_normal_bf16((T, hkv, d), dev, wl.seed, li, 0, synth.TAG_V)
+            cu = synth.cu_seqlens(self.ctx)
+            hswa.kv_append(layer, self.shape, kv.cache, k_hist, v_hist, i32(cu), i32(np.zeros(ns)))
+            k_new = synth.torch_normal_bf16((ns, hkv, d), dev, wl.seed, li, 0, synth.TAG_KDEC)
+            v_new = synth.torch_normal_bf16((ns, hkv, d), dev, wl.seed, li, 0, synth.TAG_VDEC)
+            q = synth.torch_normal_bf16((ns, hq, d), dev, wl.seed, li, 0, synth.TAG_QDEC)
+            out = torch.empty((ns, hq, d), dtype=torch.bfloat16, device=dev)
+            wsb = hswa.decode_workspace_bytes(self.shape, ns, self.maxc) if kind == "full" else 0
+            ws = torch.empty(max(1, wsb), dtype=torch.uint8, device=dev)
+            self.layers.append(dict(kind=kind, layer=layer, kv=kv, k_hist=k_hist, v_hist=v_hist, cu=cu,
+                                    k_new=k_new, v_new=v_new, q=q, out=out, ws=ws))
+        self.cu1 = i32(np.arange(ns + 1))
+        self.start = i32(self.ctx)
+        self.ctx_lens = i32(self.final)
+        torch.cuda.synchronize()
+        # algorithmic bytes
+        row = hkv * d * 2 * 2                                      # K + V bytes per key
+        qo = 2 * ns * hq * d * 2
+        self.bytes = {}
+        for L in self.layers:
+            if L["kind"] == "full":
+                keys = int(np.sum(self.ctx + 1))
+            else:
+                keys = int(np.sum(np.minimum(W, self.ctx + 1)))
+            self.bytes[L["kind"]] = keys * row + qo
+        self.append_bytes = len(self.layers) * ns * hkv * d * 2 * 2 * 2   # read + write
+
+    def step(self, full_events=None):
+        from paper_2607_13095_amd import hswa
+
+        for L in self.layers:
+            hswa.kv_append(L["layer"], self.shape, L["kv"].cache, L["k_new"], L["v_new"], self.cu1, self.start)
+            if L["kind"] == "full" and full_events is not None:
+                full_events[0].record()
+            hswa.decode(L["layer"], self.shape, L["kv"].cache, L["q"], self.ctx_lens, self.maxc, L["out"],
+                        workspace=L["ws"])
+            if L["kind"] == "full" and full_events is not None:
+                full_events[1].record()
+
+    def time_kind(self, kind, reps=20):
+        """Event timing of one layer kind's decode call alone (median of reps)."""
+        import torch
+
+        from paper_2607_13095_amd import hswa
+
+        L = next(x for x in self.layers if x["kind"] == kind)
+        ts = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            hswa.decode(L["layer"], self.shape, L["kv"].cache, L["q"], self.ctx_lens, self.maxc, L["out"],
+                        workspace=L["ws"])
+            b.record()
+            b.synchronize()
+            ts.append(a.elapsed_time(b))
+        return float(np.median(ts))
+
+    def cpu_baseline(self, target_s):
+        """fp64 oracle on the first sequences until ~target_s seconds of work."""
+        from oracle import attention as OA
+
+        threads = _blas_threads()
+        done_bytes, t_total, nseq = 0, 0.0, 0
+        row = self.wl.hkv * self.wl.head_dim * 2 * 2
+        qo = 2 * self.wl.hq * self.wl.head_dim * 2
+        for b in range(self.wl.ns):
+            for L in self.layers:
+                c = int(self.ctx[b])
+                lo = int(L["cu"][b])
+                window = self.wl.window if L["kind"] == "swa" else None
+                first = 0 if window is None else max(0, c + 1 - window)
+                # host copies of exactly the inputs the GPU read (untimed)
+                k = _host_f64(L["k_hist"][lo + first:lo + c])
+                v = _host_f64(L["v_hist"][lo + first:lo + c])
+                k = np.concatenate([k, _host_f64(L["k_new"][b:b + 1])])
+                v = np.concatenate([v, _host_f64(L["v_new"][b:b + 1])])
+                q = _host_f64(L["q"][b])
+                t0 = time.perf_counter()
+                OA.decode(q, k, v, window, self.shape.scale)
+                t_total += time.perf_counter() - t0
+                done_bytes += k.shape[0] * row + qo
+            nseq += 1
+            if t_total >= target_s:
+                break
+        return {"value": done_bytes / t_total / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
+                "sample": f"first {nseq} of {self.wl.ns} sequences, both layers, fp64 numpy oracle, "
+                          f"{t_total:.1f} s of oracle time"}
+
+
+def _host_f64(t):
+    import torch
+
+    from oracle import attention as OA
+
+    return OA.bf16_bits_to_f64(t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16))
+
+
+def _blas_threads():
+    try:
+        from threadpoolctl import threadpool_info
+
+        info = threadpool_info()
+        return int(max((i.get("num_threads", 1) for i in info if i.get("user_api") == "blas"), default=1))
+    except Exception:
+        return 1
+
+
+# ----------------------------------------------------------------------------
+# prefill workload
+# ----------------------------------------------------------------------------
+
+class PrefillBench:
+    def __init__(self, wl):
+        import torch
+
+        import synth
+        from paper_2607_13095_amd import hswa
+        from paper_2607_13095_amd.kvcache import LayerKV, pages_for
+
+        self.wl = wl
+        dev = "cuda"
+        hq, hkv, d, pg, W = wl.hq, wl.hkv, wl.head_dim, wl.page_size, wl.window
+        ns = wl.ns
+        P = np.asarray(wl.prefix, dtype=np.int64)
+        C = np.asarray(wl.new, dtype=np.int64)
+        self.P, self.C = P, C
+        final = (P + C).tolist()
+        self.shape = hswa.Shape(hq, hkv, d, pg)
+        i32 = lambda x: torch.as_tensor(np.asarray(x, dtype=np.int32), device=dev)  # noqa: E731
+        T = int(C.sum())
+        self.maxc = int(C.max())
+        self.cu = i32(synth.cu_seqlens(C))
+        self.pre = i32(P)
+        self.layers = []
+        for li, kind in enumerate(wl.layers):
+            layer = hswa.Layer.swa(W) if kind == "swa" else hswa.Layer.full()
+            npages = pages_for(layer, pg, final)
+            kv = LayerKV(layer, self.shape, final, perm=synth.page_permutation(npages, wl.seed, li))
+            kp = synth.torch_normal_bf16((int(P.sum()), hkv, d), dev, wl.seed, li, 0, synth.TAG_K)
+            vp = synth.torch_normal_bf16((int(P.sum()), hkv, d), dev, wl.seed, li, 0, synth.TAG_V)
+            hswa.kv_append(layer, self.shape, kv.cache, kp, vp, i32(synth.cu_seqlens(P)), i32(np.zeros(ns)))
+            del kp, vp
+            q = synth.torch_normal_bf16((T, hq, d), dev, wl.seed, li, 1, synth.TAG_Q)
+            kn = synth.torch_normal_bf16((T, hkv, d), dev, wl.seed, li, 1, synth.TAG_K)
+            vn = synth.torch_normal_bf16((T, hkv, d), dev, wl.seed, li, 1, synth.TAG_V)
+            out = torch.empty((T, hq, d), dtype=torch.bfloat16, device=dev)
+            self.layers.append(dict(kind=kind, layer=layer, kv=kv, q=q, kn=kn, vn=vn, out=out))
+        torch.cuda.synchronize()
+        self.flops, self.bytes = {}, {}
+        for L in self.layers:
+            pairs = 0
+            for p, c in zip(P, C):
+                if L["kind"] == "full":
+                    pairs += int(c * p + c * (c + 1) // 2)
+                else:
+                    pos = np.arange(p, p + c)
+                    pairs += int(np.minimum(W, pos + 1).sum())
+            self.flops[L["kind"]] = 4 * d * hq * pairs
+            keys = int((P + C).sum()) if L["kind"] == "full" else int(
+                sum(min(int(p), W - 1) + int(c) for p, c in zip(P, C)))
+            self.bytes[L["kind"]] = keys * hkv * d * 4 + 2 * T * hq * d * 2
+
+    def call(self, L):
+        from paper_2607_13095_amd import hswa
+
+        hswa.prefill(L["layer"], self.shape, L["kv"].cache, L["q"], L["kn"], L["vn"], self.cu, self.pre, self.maxc,
+                     L["out"])
+
+    def time_kind(self, kind, reps=10, warmup=2):
+        import torch
+
+        L = next(x for x in self.layers if x["kind"] == kind)
+        for _ in range(warmup):
+            self.call(L)
+        ts = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            self.call(L)
+            b.record()
+            b.synchronize()
+            ts.append(a.elapsed_time(b))
+        return float(np.median(ts))
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path (run with --gpus 1)",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import synth
+    from paper_2607_13095_amd import hswa
+
+    hswa.load()
+    torch.cuda.set_device(0)
+
+    wl = synth.decode_b64()
+    log(f"[bench] setting up {wl.name}")
+    db = DecodeBench(wl)
+    for _ in range(args.warmup):
+        db.step()
+    torch.cuda.synchronize()
+    full_ms = []
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    per = [[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    start.record()
+    for k in range(args.steps):
+        db.step(full_events=per[k])
+    stop.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(stop)
+    full_ms = [a.elapsed_time(b) for a, b in per]
+    ms_step = total_ms / args.steps
+    dec_bytes = sum(db.bytes.values())
+    value = dec_bytes / (ms_step * 1e-3) / 1e9
+    full_avg = float(np.mean(full_ms))
+    full_gbs = db.bytes["full"] / (full_avg * 1e-3) / 1e9
+    swa_ms = db.time_kind("swa")
+    log(f"[bench] decode step {ms_step:.4f} ms; FULL decode {full_avg:.4f} ms ({full_gbs:.0f} GB/s); "
+        f"SWA decode {swa_ms:.4f} ms")
+
+    prefill = None
+    if not args.no_prefill:
+        pw = synth.chunked_prefill_4x8k()
+        log(f"[bench] setting up {pw.name}")
+        pb = PrefillBench(pw)
+        f_ms = pb.time_kind("full")
+        s_ms = pb.time_kind("swa")
+        f_tf = pb.flops["full"] / (f_ms * 1e-3) / 1e12
+        s_gbs = pb.bytes["swa"] / (s_ms * 1e-3) / 1e9
+        prefill = {
+            "workload": pw.name, "full_ms": round(f_ms, 4), "full_tflops": round(f_tf, 2),
+            "full_frac_mfma": round(f_tf / MFMA_BF16_PEAK_TFLOPS, 4),
+            "swa_ms": round(s_ms, 4), "swa_gbs": round(s_gbs, 1), "swa_frac_hbm": round(s_gbs / HBM_PEAK_GBS, 4),
+            "swa_tflops": round(pb.flops["swa"] / (s_ms * 1e-3) / 1e12, 2),
+            "roofline": {"bound": "mfma", "achieved": round(f_tf, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
+                         "unit": "TFLOP/s", "frac": round(f_tf / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None},
+        }
+        log(f"[bench] prefill FULL {f_ms:.3f} ms = {f_tf:.1f} TFLOP/s; SWA {s_ms:.3f} ms = {s_gbs:.0f} GB/s")
+        del pb
+        torch.cuda.empty_cache()
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("[bench] CPU baseline (oracle)")
+        cpu = db.cpu_baseline(args.cpu_seconds)
+
+    line = {
+        "metric": "decode attn HBM GB/s (% peak) + prefill attn TFLOP/s (% MFMA), W=128",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "sequences": wl.ns, "context": "uniform [1024, 32768] cached tokens",
+                   "layers": "1 SWA (W=128) + 1 FULL", "q_heads": wl.hq, "kv_heads": wl.hkv,
+                   "head_dim": wl.head_dim, "page_size": wl.page_size, "frac_hbm": round(value / HBM_PEAK_GBS, 4),
+                   "decode_bytes": dec_bytes, "full_decode_ms": round(full_avg, 5),
+                   "swa_decode_ms": round(swa_ms, 5)},
+        "roofline": {"bound": "hbm", "achieved": round(full_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(full_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": "FULL-layer decode (split-KV + merge)"},
+        "prefill": prefill,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()
