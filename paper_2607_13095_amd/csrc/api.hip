@@ -20,10 +20,7 @@ bool sync_check_enabled() {
 
 hswa_status finish_launch(hipError_t e, hipStream_t stream) {
   if (e != hipSuccess) return HSWA_ERR_LAUNCH;
-  if (sync_check_enabled()) {
-    if (hipStreamSynchronize(stream) != hipSuccess) return HSWA_ERR_LAUNCH;
-    if (hipGetLastError() != hipSuccess) return HSWA_ERR_LAUNCH;
-  }
+  if (sync_check_enabled() && hipStreamSynchronize(stream) != hipSuccess) return HSWA_ERR_LAUNCH;
   return HSWA_OK;
 }
 

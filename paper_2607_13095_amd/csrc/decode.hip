@@ -4,237 +4,337 @@
 // bytes read; SWA layers read at most W keys from the per-sequence ring, FULL
 // layers read the whole context.
 //
-// Work unit: one workgroup (4 waves) per (key range, KV head, sequence, group of
-// up to 16 query heads of that KV head). Every wave walks 32-key chunks of the
-// range and runs both products on the bf16 matrix cores with the GQA query
-// heads as the 16 MFMA columns:
+// Work item: one wavefront per (sequence, KV head, group of up to 16 query heads
+// of that KV head, key range). An SWA layer (or a FULL layer short enough for
+// one piece) has one item per (sequence, head group) covering every visible key;
+// a FULL layer splits the context into pieces of split_len keys. Workgroups are
+// single waves, one item each; split items are numbered over the pieces that
+// exist, so the dispatcher balances the uneven sequence lengths by itself.
+//
+// Per item the wave walks 32-key chunks and runs both products on the bf16
+// matrix cores with the GQA query heads as the 16 MFMA columns:
 //   S^T[key][head]  = K[key][:] . Q[head][:]        (K rows straight from HBM)
 //   O^T[d][head]   += V^T[d][key] . P^T[key][head]   (V pages are stored [D][PG])
 // The 32 keys of a chunk are assigned to MFMA rows so that the score tile comes
 // out with each lane holding 8 consecutive keys of one head, which is exactly
 // the lane layout the PV product needs for P^T: no shuffle between the two.
 // Softmax is online per chunk in fp32 (exp2 with scale*log2(e) folded in).
-// The 4 waves are merged through LDS at the end. A FULL layer whose context is
-// split into several pieces writes fp32 (o, log2-sum-exp) partials that a second
-// kernel merges; an SWA layer (or a single piece) writes bf16 output directly.
+// The K loads of chunk c+1 are in flight while chunk c's softmax and PV run,
+// its V loads while chunk c+1's QK^T runs. A split item writes fp32 (o, log2
+// sum-exp) partials that a second kernel merges; a whole-range item writes bf16.
 #include "hswa_common.h"
 #include "hswa_launch.h"
 
 namespace hswa {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kWaves = kThreads / kWave;
 constexpr int kChunk = 32;
-constexpr int kCols = 16;        // query heads per workgroup (MFMA columns)
-constexpr int kORow = kHeadDim + 4;
+constexpr int kCols = 16;  // query heads per item (MFMA columns)
+constexpr int kMergeThreads = 256;
 
-__device__ __forceinline__ int64_t lookup_page(const PoolView &pv, int b, int key, bool &ok) {
-  int lp = key >> pv.pg_shift;
-  if (pv.ring > 0) lp %= pv.ring;
-  const int64_t page = pv.table[(int64_t)b * pv.stride + lp];
-  ok = page >= 0 && page < pv.num_pages;
-  return ok ? page : 0;
+// Per-wave copy of a window of the block table: lane i holds the physical page
+// of logical page lp0 + i (-1 if outside the range or not a valid page id), so
+// page ids are read with v_readlane instead of a dependent global load per chunk.
+struct LaneTable {
+  int page;
+  int lp0;
+};
+
+__device__ __forceinline__ void load_lane_table(LaneTable &t, const PoolView &pv, int b, int lp0, int last_lp,
+                                                int lane) {
+  t.lp0 = lp0;
+  const int lp = lp0 + lane;
+  int page = -1;
+  if (lp <= last_lp) {
+    const int e = pv.ring > 0 ? lp % pv.ring : lp;
+    const int64_t v = pv.table[(int64_t)b * pv.stride + e];
+    page = (v >= 0 && v < pv.num_pages) ? (int)v : -1;
+  }
+  t.page = page;
 }
 
-template <bool kSplit>
-__global__ __launch_bounds__(kThreads) void decode_kernel(DecodeParams p) {
-  __shared__ float s_m[kWaves][kCols];
-  __shared__ float s_l[kWaves][kCols];
-  __shared__ __attribute__((aligned(16))) float s_o[kWaves][kCols][kORow];
+// Operands of one 32-key chunk, loaded ahead of their use.
+struct Chunk {
+  u32x4 ka[4], kb[4], v[8];
+  int kv0;
+  bool vok;
+};
 
+template <bool kSplit, bool kOnePage>
+__global__ __launch_bounds__(kWave) void decode_kernel(DecodeParams p) {
   const PoolView &pv = p.pool;
-  const int split = blockIdx.x;
-  const int hchunks = (p.group + kCols - 1) / kCols;
-  const int g = blockIdx.y / hchunks;
-  const int hc = blockIdx.y - g * hchunks;
-  const int b = blockIdx.z;
-  const int tid = threadIdx.x;
-  const int lane = tid & (kWave - 1), wave = tid / kWave;
+  const int lane = threadIdx.x;
   const int r = lane & 15, q = lane >> 4;
-  const int nheads = min(kCols, p.group - hc * kCols);
-  const int head0 = g * p.group + hc * kCols;
   const int hkv = p.hkv;
   const int shift = pv.pg_shift;
   const int pg = 1 << shift;
+  const float c2 = p.scale_log2;
+  const int hchunks = (p.group + kCols - 1) / kCols;
 
-  const int ctx = min(p.ctx_lens[b], p.max_ctx);
-  if (ctx < 1) {
-    if (!kSplit) {
-      for (int i = tid; i < nheads * (kHeadDim / 2); i += kThreads) {
-        const int h = i / (kHeadDim / 2), dp = i - h * (kHeadDim / 2);
-        reinterpret_cast<uint32_t *>(p.out + ((int64_t)b * p.hq + head0 + h) * kHeadDim)[dp] = 0u;
+  // Loop-invariant byte offsets of this lane's operands inside one page-head
+  // (used when a 32-key chunk never straddles two pages, i.e. PG >= 32).
+  const uint32_t koff_a = ((8 * (r >> 2) + (r & 3)) * kHeadDim + 8 * q) * 2;
+  const uint32_t koff_b = koff_a + 4 * kHeadDim * 2;
+  const uint32_t voff = ((uint32_t)r << shift) * 2 + 16 * q;
+  const uint32_t vstep = (16u << shift) * 2;  // 16 dims of V^T
+
+  // Which item this workgroup runs. Split items are numbered over the pieces
+  // that exist (sequence by sequence, piece by piece, head group fastest), so
+  // every launched workgroup up to the real item count has work and the
+  // surplus of the upper-bound grid exits at once.
+  const int H = hkv * hchunks;
+  const int gy = (int)(blockIdx.x % H);
+  int b = 0, split = 0;
+  if constexpr (kSplit) {
+    const int64_t j = blockIdx.x / H;  // index of the (sequence, piece) pair
+    int64_t base = 0;
+    b = -1;
+    for (int b0 = 0; b0 < p.ns; b0 += kWave) {
+      const int bb = b0 + lane;
+      int n = 0;
+      if (bb < p.ns) {
+        const int c = min(p.ctx_lens[bb], p.max_ctx);
+        n = c >= 1 ? (c - 1) / p.split_len + 1 : 0;
+      }
+      int incl = n;  // inclusive prefix sum of piece counts across the wave
+#pragma unroll
+      for (int off = 1; off < kWave; off <<= 1) {
+        const int t = __shfl_up(incl, off, kWave);
+        if (lane >= off) incl += t;
+      }
+      const int tot = __shfl(incl, kWave - 1, kWave);
+      if (j < base + tot) {
+        const uint64_t hit = __ballot(base + incl > j);
+        const int first = __builtin_ctzll(hit);
+        const int excl = __shfl(incl - n, first, kWave);
+        b = b0 + first;
+        split = (int)(j - base - excl);
+        break;
+      }
+      base += tot;
+    }
+    if (b < 0) return;
+  } else {
+    b = (int)(blockIdx.x / H);
+  }
+  {
+    const int g = gy / hchunks;
+    const int hc = gy - g * hchunks;
+    const int nheads = min(kCols, p.group - hc * kCols);
+    const int head0 = g * p.group + hc * kCols;
+    const int64_t row = (int64_t)b * p.hq + head0 + r;  // this lane's output row (if r < nheads)
+
+    const int ctx = min(p.ctx_lens[b], p.max_ctx);
+    if (ctx < 1) {
+      if (!kSplit && r < nheads) {
+        const u32x2 z = {0u, 0u};
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) *reinterpret_cast<u32x2 *>(p.out + row * kHeadDim + 16 * dt + 4 * q) = z;
+      }
+      return;
+    }
+    const int pos = ctx - 1;
+    int kb, ke;
+    if (kSplit) {
+      kb = split * p.split_len;
+      ke = min(pos, kb + p.split_len - 1);
+    } else {
+      kb = pv.window > 0 ? max(0, pos - pv.window + 1) : 0;
+      ke = pos;
+    }
+
+    // Q^T operand: lane holds head r, dims 32t + 8q .. +7 for step t.
+    u32x4 qf[4];
+    {
+      const bool hv = r < nheads;
+      const uint16_t *qrow = p.q + ((int64_t)b * p.hq + head0 + (hv ? r : 0)) * kHeadDim;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const u32x4 v = ldg128(qrow + 32 * t + 8 * q);
+        const u32x4 z = {0u, 0u, 0u, 0u};
+        qf[t] = hv ? v : z;
       }
     }
-    return;
-  }
-  const int pos = ctx - 1;
-  int kb, ke;
-  if (kSplit) {
-    kb = split * p.split_len;
-    if (kb > pos) return;
-    ke = min(pos, kb + p.split_len - 1);
-  } else {
-    kb = pv.window > 0 ? max(0, pos - pv.window + 1) : 0;
-    ke = pos;
-  }
 
-  // Q^T operand: lane holds head r, dims 32t + 8q .. +7 for step t.
-  u32x4 qf[4];
-  {
-    const bool hv = r < nheads;
-    const uint16_t *qrow = p.q + ((int64_t)b * p.hq + head0 + (hv ? r : 0)) * kHeadDim;
+    const int cfirst = kb & ~(kChunk - 1);
+    const int nchunks = ((ke - cfirst) >> 5) + 1;
+    const int klo8 = kb & ~7, khi8 = ke & ~7;
+    const int last_lp = ke >> shift;
+
+    LaneTable tab;
+    load_lane_table(tab, pv, b, kb >> shift, last_lp, lane);
+
+    float m = -INFINITY, lsum = 0.f;
+    f32x4 acc[8];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const u32x4 v = ldg128(qrow + 32 * t + 8 * q);
-      const u32x4 z = {0u, 0u, 0u, 0u};
-      qf[t] = hv ? v : z;
-    }
-  }
+    for (int i = 0; i < 8; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const float c2 = p.scale_log2;
-  const int cfirst = kb & ~(kChunk - 1);
-  const int nchunks = ((ke - cfirst) >> 5) + 1;
-  const int klo8 = kb & ~7, khi8 = ke & ~7;
-
-  float m = -INFINITY, lsum = 0.f;
-  f32x4 acc[8];
+    auto issue_k = [&](int c, int page, Chunk &ch) {
+      const int cbase = cfirst + c * kChunk;
+      const int64_t pg64 = max(page, 0);
+      const char *kbase = reinterpret_cast<const char *>(pv.k_pool) +
+                          ((((pg64 * hkv + g) << shift) + (cbase & (pg - 1))) * kHeadDim) * 2;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  for (int c = wave; c < nchunks; c += kWaves) {
-    const int cbase = cfirst + c * kChunk;
-    // K rows of this lane: keys cbase + 8*(r/4) + (r%4) (+4 for the second tile)
-    const int ka = min(max(cbase + 8 * (r >> 2) + (r & 3), kb), ke);
-    const int kb2 = min(max(cbase + 8 * (r >> 2) + 4 + (r & 3), kb), ke);
-    const int kv0 = cbase + 8 * q;                  // the 8 keys whose scores / V this lane holds
-    const int kvg = min(max(kv0, klo8), khi8);
-    bool oka, okb, okv;
-    const int64_t pa = lookup_page(pv, b, ka, oka);
-    const int64_t pb = lookup_page(pv, b, kb2, okb);
-    const int64_t pvv = lookup_page(pv, b, kvg, okv);
-
-    const uint16_t *krow_a = pv.k_pool + (((pa * hkv + g) << shift) + (ka & (pg - 1))) * kHeadDim;
-    const uint16_t *krow_b = pv.k_pool + (((pb * hkv + g) << shift) + (kb2 & (pg - 1))) * kHeadDim;
-    const uint16_t *vcol = pv.v_pool + ((pvv * hkv + g) * kHeadDim << shift) + (kvg & (pg - 1));
-
-    u32x4 kfa[4], kfb[4], vf[8];
+      for (int t = 0; t < 4; ++t) {
+        ch.ka[t] = ldg128(kbase + koff_a + 64 * t);
+        ch.kb[t] = ldg128(kbase + koff_b + 64 * t);
+      }
+    };
+    auto issue_v = [&](int c, int page, Chunk &ch) {
+      const int cbase = cfirst + c * kChunk;
+      const int64_t pg64 = max(page, 0);
+      const char *vbase = reinterpret_cast<const char *>(pv.v_pool) +
+                          ((((pg64 * hkv + g) * kHeadDim) << shift) + (cbase & (pg - 1))) * 2;
+      ch.kv0 = cbase + 8 * q;
+      ch.vok = page >= 0;
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      kfa[t] = ldg128(krow_a + 32 * t + 8 * q);
-      kfb[t] = ldg128(krow_b + 32 * t + 8 * q);
-    }
+      for (int dt = 0; dt < 8; ++dt) ch.v[dt] = ldg128(vbase + voff + dt * vstep);
+    };
+    // General path (PG = 16: a chunk spans two pages): per-lane page choice.
+    auto issue = [&](int c, Chunk &ch) {
+      const int cbase = cfirst + c * kChunk;
+      const int lpc = max(cbase, kb) >> shift;  // first page of the chunk's valid keys
+      if ((min(cbase + kChunk - 1, ke) >> shift) - tab.lp0 >= kWave) load_lane_table(tab, pv, b, lpc, last_lp, lane);
+      const int rel = lpc - tab.lp0;
+      const int pg0 = __builtin_amdgcn_readlane(tab.page, rel);
+      const int pg1 = __builtin_amdgcn_readlane(tab.page, min(rel + 1, kWave - 1));
+      const int ka = min(max(cbase + 8 * (r >> 2) + (r & 3), kb), ke);
+      const int kb2 = min(max(cbase + 8 * (r >> 2) + 4 + (r & 3), kb), ke);
+      const int kvg = min(max(cbase + 8 * q, klo8), khi8);
+      const int pa = (ka >> shift) == lpc ? pg0 : pg1;
+      const int pb = (kb2 >> shift) == lpc ? pg0 : pg1;
+      const int pvv = (kvg >> shift) == lpc ? pg0 : pg1;
+      ch.kv0 = cbase + 8 * q;
+      ch.vok = pvv >= 0;
+      const int64_t pa64 = max(pa, 0), pb64 = max(pb, 0), pv64 = max(pvv, 0);
+      const uint16_t *krow_a = pv.k_pool + (((pa64 * hkv + g) << shift) + (ka & (pg - 1))) * kHeadDim;
+      const uint16_t *krow_b = pv.k_pool + (((pb64 * hkv + g) << shift) + (kb2 & (pg - 1))) * kHeadDim;
+      const uint16_t *vcol = pv.v_pool + ((pv64 * hkv + g) * kHeadDim << shift) + (kvg & (pg - 1));
 #pragma unroll
-    for (int dt = 0; dt < 8; ++dt) vf[dt] = ldg128(vcol + ((int64_t)(16 * dt + r) << shift));
-
-    f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
+      for (int t = 0; t < 4; ++t) {
+        ch.ka[t] = ldg128(krow_a + 32 * t + 8 * q);
+        ch.kb[t] = ldg128(krow_b + 32 * t + 8 * q);
+      }
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      sa = mfma16x16x32(kfa[t], qf[t], sa);
-      sb = mfma16x16x32(kfb[t], qf[t], sb);
-    }
+      for (int dt = 0; dt < 8; ++dt) ch.v[dt] = ldg128(vcol + ((int64_t)(16 * dt + r) << shift));
+    };
 
+    // QK^T and the online softmax of one chunk: returns P^T packed as bf16 and
+    // leaves the rescale factor in `alpha` and the key mask in `keep`.
+    float alpha = 1.f;
     uint32_t keep = 0;
+    auto scores = [&](Chunk &ch) {
+      f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int i = 0; i < 8; ++i) keep |= (uint32_t)(kv0 + i >= kb && kv0 + i <= ke) << i;
-    if (!okv) keep = 0;
+      for (int t = 0; t < 4; ++t) {
+        sa = mfma16x16x32(ch.ka[t], qf[t], sa);
+        sb = mfma16x16x32(ch.kb[t], qf[t], sb);
+      }
+      keep = 0;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) keep |= (uint32_t)(ch.kv0 + i >= kb && ch.kv0 + i <= ke) << i;
+      if (!ch.vok) keep = 0;
+      float s[8];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        s[i] = (keep >> i) & 1u ? sa[i] : -INFINITY;
+        s[4 + i] = (keep >> (4 + i)) & 1u ? sb[i] : -INFINITY;
+      }
+      float cmax = s[0];
+#pragma unroll
+      for (int i = 1; i < 8; ++i) cmax = fmaxf(cmax, s[i]);
+      cmax = wave_max_xor(cmax, 16);
+      cmax = wave_max_xor(cmax, 32);
+      const float mnew = fmaxf(m, cmax);
+      const float mc = mnew == -INFINITY ? 0.f : mnew * c2;
+      alpha = fast_exp2(m * c2 - mc);
+      float pr[8], psum = 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        pr[i] = fast_exp2(fmaf(s[i], c2, -mc));
+        psum += pr[i];
+      }
+      lsum = lsum * alpha + psum;
+      m = mnew;
+      u32x4 pf;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) pf[j] = pack_bf16x2(pr[2 * j], pr[2 * j + 1]);
+      return pf;
+    };
+    auto pv_update = [&](Chunk &ch, u32x4 pf) {
+      if (keep != 0xFFu) {
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) ch.v[dt] = keep_bf16x8(ch.v[dt], keep);
+      }
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) {
+        acc[dt] *= alpha;
+        acc[dt] = mfma16x16x32(ch.v[dt], pf, acc[dt]);
+      }
+    };
 
-    float s[8];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      s[i] = (keep >> i) & 1u ? sa[i] : -INFINITY;
-      s[4 + i] = (keep >> (4 + i)) & 1u ? sb[i] : -INFINITY;
-    }
-    float cmax = s[0];
-#pragma unroll
-    for (int i = 1; i < 8; ++i) cmax = fmaxf(cmax, s[i]);
-    cmax = wave_max_xor(cmax, 16);
-    cmax = wave_max_xor(cmax, 32);
-    const float mnew = fmaxf(m, cmax);
-    const float mc = mnew == -INFINITY ? 0.f : mnew * c2;
-    const float alpha = fast_exp2(m * c2 - mc);
-    float pr[8], psum = 0.f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      pr[i] = fast_exp2(fmaf(s[i], c2, -mc));
-      psum += pr[i];
-    }
-    lsum = lsum * alpha + psum;
-    m = mnew;
-
-    u32x4 pf;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) pf[j] = pack_bf16x2(pr[2 * j], pr[2 * j + 1]);
-    if (keep != 0xFFu) {
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) vf[dt] = keep_bf16x8(vf[dt], keep);
-    }
-#pragma unroll
-    for (int dt = 0; dt < 8; ++dt) {
-      acc[dt] *= alpha;
-      acc[dt] = mfma16x16x32(vf[dt], pf, acc[dt]);
-    }
-  }
-
-  // Merge the 4 waves.
-  lsum = wave_sum_xor(lsum, 16);
-  lsum = wave_sum_xor(lsum, 32);
-  if (q == 0) {
-    s_m[wave][r] = m;
-    s_l[wave][r] = lsum;
-  }
-  __syncthreads();
-  float mall = s_m[0][r];
-#pragma unroll
-  for (int w = 1; w < kWaves; ++w) mall = fmaxf(mall, s_m[w][r]);
-  const float f = m == -INFINITY ? 0.f : fast_exp2((m - mall) * c2);
-#pragma unroll
-  for (int dt = 0; dt < 8; ++dt) {
-    f32x4 v = acc[dt] * f;
-    *reinterpret_cast<f32x4 *>(&s_o[wave][r][16 * dt + 4 * q]) = v;
-  }
-  __syncthreads();
-
-  // Thread -> (head h, dims 2*(tid%16) + 32*k).
-  const int h = tid >> 4;
-  if (h >= nheads) return;
-  float mh = s_m[0][h];
-#pragma unroll
-  for (int w = 1; w < kWaves; ++w) mh = fmaxf(mh, s_m[w][h]);
-  float fw[kWaves], ltot = 0.f;
-#pragma unroll
-  for (int w = 0; w < kWaves; ++w) {
-    fw[w] = s_m[w][h] == -INFINITY ? 0.f : fast_exp2((s_m[w][h] - mh) * c2);
-    ltot += fw[w] * s_l[w][h];
-  }
-  const float inv = 1.f / ltot;
-  const int64_t row = (int64_t)b * p.hq + head0 + h;
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const int d = 2 * (tid & 15) + 32 * k;
-    float o0 = 0.f, o1 = 0.f;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-      o0 += s_o[w][h][d];
-      o1 += s_o[w][h][d + 1];
-    }
-    o0 *= inv;
-    o1 *= inv;
-    if (kSplit) {
-      float *dst = p.ws_o + (row * p.max_splits + split) * kHeadDim + d;
-      dst[0] = o0;
-      dst[1] = o1;
+    // The one-page path needs every page of the range in the lane table; the
+    // host only selects it when every range spans fewer than 64 pages.
+    if constexpr (kOnePage) {
+      // Rolling prefetch with one register set; the last chunk is peeled so
+      // that the loop body always prefetches (uniform wait counts).
+      auto page_of = [&](int c) {
+        return __builtin_amdgcn_readlane(tab.page, ((cfirst + c * kChunk) >> shift) - tab.lp0);
+      };
+      Chunk ch;
+      {
+        const int page = page_of(0);
+        issue_k(0, page, ch);
+        issue_v(0, page, ch);
+      }
+      for (int c = 0; c < nchunks - 1; ++c) {
+        const int next_page = page_of(c + 1);
+        const u32x4 pf = scores(ch);
+        issue_k(c + 1, next_page, ch);
+        pv_update(ch, pf);
+        issue_v(c + 1, next_page, ch);
+      }
+      const u32x4 pf = scores(ch);
+      pv_update(ch, pf);
     } else {
-      reinterpret_cast<uint32_t *>(p.out + row * kHeadDim)[d >> 1] = pack_bf16x2(o0, o1);
+      for (int c = 0; c < nchunks; ++c) {
+        Chunk ch;
+        issue(c, ch);
+        const u32x4 pf = scores(ch);
+        pv_update(ch, pf);
+      }
+    }
+
+    // Normalise and write: lane holds O^T[d = 16 dt + 4 q + i][head r].
+    lsum = wave_sum_xor(lsum, 16);
+    lsum = wave_sum_xor(lsum, 32);
+    if (r < nheads) {
+      const float inv = 1.f / lsum;
+      if (kSplit) {
+        float *dst = p.ws_o + (row * p.max_splits + split) * kHeadDim + 4 * q;
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) *reinterpret_cast<f32x4 *>(dst + 16 * dt) = acc[dt] * inv;
+        if (q == 0) p.ws_lse[row * p.max_splits + split] = m * c2 + __log2f(lsum);
+      } else {
+        uint16_t *dst = p.out + row * kHeadDim + 4 * q;
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) {
+          u32x2 w;
+          w[0] = pack_bf16x2(acc[dt][0] * inv, acc[dt][1] * inv);
+          w[1] = pack_bf16x2(acc[dt][2] * inv, acc[dt][3] * inv);
+          *reinterpret_cast<u32x2 *>(dst + 16 * dt) = w;
+        }
+      }
     }
   }
-  if (kSplit && (tid & 15) == 0) p.ws_lse[row * p.max_splits + split] = mh * c2 + __log2f(ltot);
 }
 
 // Log-sum-exp merge of the split partials: one wave per (sequence, query head).
-__global__ __launch_bounds__(kThreads) void decode_merge_kernel(DecodeParams p) {
+// Lane j reads the log-sum-exp of pieces j, j+64, ...; the weights are then
+// broadcast piece by piece while every lane accumulates two output dims.
+__global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(DecodeParams p) {
   const int lane = threadIdx.x & (kWave - 1);
-  const int64_t idx = (int64_t)blockIdx.x * kWaves + (threadIdx.x / kWave);
+  const int64_t idx = (int64_t)blockIdx.x * (kMergeThreads / kWave) + (threadIdx.x / kWave);
   if (idx >= (int64_t)p.ns * p.hq) return;
   const int b = (int)(idx / p.hq);
   const int ctx = min(p.ctx_lens[b], p.max_ctx);
@@ -246,14 +346,22 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(DecodeParams p) 
   const int nsplit = (ctx - 1) / p.split_len + 1;
   const float *lse = p.ws_lse + idx * p.max_splits;
   float mx = -INFINITY;
-  for (int s = 0; s < nsplit; ++s) mx = fmaxf(mx, lse[s]);
-  float wsum = 0.f, o0 = 0.f, o1 = 0.f;
+  for (int s = lane; s < nsplit; s += kWave) mx = fmaxf(mx, lse[s]);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, kWave));
   const float *po = p.ws_o + idx * p.max_splits * kHeadDim + 2 * lane;
-  for (int s = 0; s < nsplit; ++s) {
-    const float w = fast_exp2(lse[s] - mx);
-    wsum += w;
-    o0 = fmaf(w, po[(int64_t)s * kHeadDim], o0);
-    o1 = fmaf(w, po[(int64_t)s * kHeadDim + 1], o1);
+  float wsum = 0.f, o0 = 0.f, o1 = 0.f;
+  for (int s0 = 0; s0 < nsplit; s0 += kWave) {
+    const int s = s0 + lane;
+    const float w = s < nsplit ? fast_exp2(lse[s] - mx) : 0.f;
+    const int n = min(kWave, nsplit - s0);
+    for (int k = 0; k < n; ++k) {
+      const float wk = __shfl(w, k, kWave);
+      const float2 v = *reinterpret_cast<const float2 *>(po + (int64_t)(s0 + k) * kHeadDim);
+      wsum += wk;
+      o0 = fmaf(wk, v.x, o0);
+      o1 = fmaf(wk, v.y, o1);
+    }
   }
   const float inv = 1.f / wsum;
   *dst = pack_bf16x2(o0 * inv, o1 * inv);
@@ -262,10 +370,14 @@ __global__ __launch_bounds__(kThreads) void decode_merge_kernel(DecodeParams p) 
 }  // namespace
 
 int32_t decode_split_len(int32_t ns, int32_t hkv, int32_t group, int32_t max_ctx) {
-  const int64_t units = (int64_t)ns * hkv * ((group + kCols - 1) / kCols);
-  int32_t len = 1024;
-  while (len > 256 && units * ((max_ctx + len - 1) / len) < 2048) len /= 2;
-  // keep the number of pieces bounded for very long contexts
+  // Aim for about 8192 wave items when contexts average half the maximum
+  // (a few per resident wave, so the dispatcher can balance uneven lengths),
+  // with pieces of 256 to 2048 keys; very long contexts get longer pieces so
+  // that the piece count stays at most 256.
+  const int64_t heads = (int64_t)hkv * ((group + kCols - 1) / kCols);
+  const int64_t keys = heads * ns * (int64_t)max_ctx / 2;
+  int32_t len = 256;
+  while (len < 2048 && keys / (2 * len) >= 8192) len *= 2;
   const int64_t min_len = ((int64_t)max_ctx + 255) / 256;
   while (len < min_len) len *= 2;
   return len;
@@ -274,18 +386,25 @@ int32_t decode_split_len(int32_t ns, int32_t hkv, int32_t group, int32_t max_ctx
 hipError_t launch_decode(const DecodeParams &p, hipStream_t stream) {
   if (p.ns <= 0) return hipSuccess;
   const int hchunks = (p.group + kCols - 1) / kCols;
-  const dim3 grid(p.max_splits, p.hkv * hchunks, p.ns);
+  const int64_t items = (int64_t)p.ns * p.hkv * hchunks * p.max_splits;  // upper bound
+  const unsigned grid = (unsigned)items;
+  // One-page path: 32-key chunks never straddle pages (PG >= 32) and every key
+  // range fits the 64-entry lane table.
+  const int64_t range = p.max_splits > 1 ? p.split_len
+                                         : (p.pool.window > 0 ? min(p.pool.window, p.max_ctx) : p.max_ctx);
+  const int64_t range_pages = ((range + (1 << p.pool.pg_shift) - 1) >> p.pool.pg_shift) + 1;
+  const bool one_page = p.pool.pg_shift >= 5 && range_pages < kWave;
   if (p.max_splits > 1) {
-    hipLaunchKernelGGL(decode_kernel<true>, grid, dim3(kThreads), 0, stream, p);
-    hipError_t e = hipGetLastError();
+    const hipError_t e = one_page ? launch_kernel(decode_kernel<true, true>, dim3(grid), dim3(kWave), stream, p)
+                                  : launch_kernel(decode_kernel<true, false>, dim3(grid), dim3(kWave), stream, p);
     if (e != hipSuccess) return e;
     const int64_t rows = (int64_t)p.ns * p.hq;
-    hipLaunchKernelGGL(decode_merge_kernel, dim3((unsigned)((rows + kWaves - 1) / kWaves)), dim3(kThreads), 0,
-                       stream, p);
-  } else {
-    hipLaunchKernelGGL(decode_kernel<false>, grid, dim3(kThreads), 0, stream, p);
+    const int per_block = kMergeThreads / kWave;
+    return launch_kernel(decode_merge_kernel, dim3((unsigned)((rows + per_block - 1) / per_block)),
+                         dim3(kMergeThreads), stream, p);
   }
-  return hipGetLastError();
+  return one_page ? launch_kernel(decode_kernel<false, true>, dim3(grid), dim3(kWave), stream, p)
+                  : launch_kernel(decode_kernel<false, false>, dim3(grid), dim3(kWave), stream, p);
 }
 
 }  // namespace hswa

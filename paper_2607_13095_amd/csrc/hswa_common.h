@@ -69,4 +69,14 @@ __device__ __forceinline__ float wave_sum_xor(float v, int mask) { return v + __
 
 constexpr float kLog2e = 1.4426950408889634f;
 
+// Launch a kernel taking one parameter struct and return the status of exactly
+// this launch (hipGetLastError would also report errors left behind by earlier,
+// unrelated runtime calls of the caller).
+template <typename Params>
+inline hipError_t launch_kernel(void (*kernel)(Params), dim3 grid, dim3 block, hipStream_t stream,
+                                const Params &p) {
+  void *args[] = {const_cast<Params *>(&p)};
+  return hipLaunchKernel(reinterpret_cast<const void *>(kernel), grid, block, args, 0, stream);
+}
+
 }  // namespace hswa

@@ -5,11 +5,11 @@
 // and the ring overwrite is the out-of-window eviction that follows every chunk
 // and every decode step ("SWA-Aware Prefix Cache Tree").
 //
-// One workgroup handles 8 consecutive tokens of the flattened batch. The K row
-// of a token is one contiguous 256-byte run per KV head in the pool; V pages
-// are stored transposed ([D][PG] per head), so 8 tokens that land on 8
-// consecutive, 8-aligned slots of one page are written as one 16-byte store
-// per (head, dim); anything else falls back to 2-byte stores.
+// One workgroup handles 8 consecutive tokens of the flattened batch for one KV
+// head. The K row of a token is one contiguous 256-byte run per KV head in the
+// pool; V pages are stored transposed ([D][PG] per head), so 8 tokens that land
+// on 8 consecutive, 8-aligned slots of one page are written as one 16-byte
+// store per dim; anything else falls back to 2-byte stores.
 #include "hswa_common.h"
 #include "hswa_launch.h"
 
@@ -50,44 +50,46 @@ __device__ int64_t slot_of_token(const AppendParams &p, int t) {
   return page * pg + (j & (pg - 1));
 }
 
+// Grid: (groups of 8 tokens, KV heads). Each workgroup moves 8 tokens of one
+// KV head: 8 K rows of 256 bytes and 8 x 128 V values.
 __global__ __launch_bounds__(kThreads) void kv_append_kernel(AppendParams p) {
   __shared__ int64_t s_slot[kTokPerBlock];
   const int t0 = blockIdx.x * kTokPerBlock;
+  const int g = blockIdx.y;
   const int tid = threadIdx.x;
   const int ntok = min(kTokPerBlock, p.total_tokens - t0);
   if (tid < ntok) {
     const int64_t s = slot_of_token(p, t0 + tid);
     s_slot[tid] = s;
-    if (p.slot_out) p.slot_out[t0 + tid] = s;
+    if (p.slot_out && g == 0) p.slot_out[t0 + tid] = s;
   }
   __syncthreads();
 
   const PoolView &pv = p.pool;
   const int pg = 1 << pv.pg_shift;
   const int hkv = p.hkv;
-  const int row16 = kHeadDim / 8;  // 16-byte pieces per K row
+  constexpr int kRow16 = kHeadDim / 8;  // 16-byte pieces per K row
 
-  // K rows: contiguous per (page, head, offset).
-  for (int i = tid; i < ntok * hkv * row16; i += kThreads) {
-    const int tok = i / (hkv * row16);
-    const int rem = i - tok * hkv * row16;
-    const int g = rem / row16, c = rem - g * row16;
-    const int64_t s = s_slot[tok];
-    if (s < 0) continue;
-    const int64_t page = s >> pv.pg_shift, off = s & (pg - 1);
-    const u32x4 v = ldg128(p.k_new + ((int64_t)(t0 + tok) * hkv + g) * kHeadDim + c * 8);
-    stg128(pv.k_pool + ((page * hkv + g) * pg + off) * kHeadDim + c * 8, v);
+  // K rows: contiguous per (page, head, offset); threads 0..127 copy 8 rows.
+  if (tid < kTokPerBlock * kRow16) {
+    const int tok = tid / kRow16, c = tid % kRow16;
+    const int64_t s = tok < ntok ? s_slot[tok] : -1;
+    if (s >= 0) {
+      const int64_t page = s >> pv.pg_shift, off = s & (pg - 1);
+      const u32x4 v = ldg128(p.k_new + ((int64_t)(t0 + tok) * hkv + g) * kHeadDim + c * 8);
+      stg128(pv.k_pool + ((page * hkv + g) * pg + off) * kHeadDim + c * 8, v);
+    }
   }
 
   // V: transposed pages.
   bool run = ntok == kTokPerBlock && s_slot[0] >= 0 && (s_slot[0] & 7) == 0;
 #pragma unroll
   for (int i = 1; i < kTokPerBlock; ++i) run = run && s_slot[i] == s_slot[0] + i;
-  const int nvec = hkv * kHeadDim;
   if (run) {
-    const int64_t page = s_slot[0] >> pv.pg_shift, off = s_slot[0] & (pg - 1);
-    for (int e = tid; e < nvec; e += kThreads) {
-      const int g = e / kHeadDim, d = e - g * kHeadDim;
+    // 8 consecutive, 8-aligned slots of one page: one 16-byte store per dim
+    if (tid < kHeadDim) {
+      const int d = tid;
+      const int64_t page = s_slot[0] >> pv.pg_shift, off = s_slot[0] & (pg - 1);
       const uint16_t *src = p.v_new + ((int64_t)t0 * hkv + g) * kHeadDim + d;
       u32x4 w;
 #pragma unroll
@@ -99,10 +101,8 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(AppendParams p) {
       stg128(pv.v_pool + ((page * hkv + g) * kHeadDim + d) * pg + off, w);
     }
   } else {
-    for (int i = tid; i < ntok * nvec; i += kThreads) {
-      const int tok = i / nvec;
-      const int e = i - tok * nvec;
-      const int g = e / kHeadDim, d = e - g * kHeadDim;
+    for (int i = tid; i < ntok * kHeadDim; i += kThreads) {
+      const int tok = i / kHeadDim, d = i - tok * kHeadDim;
       const int64_t s = s_slot[tok];
       if (s < 0) continue;
       const int64_t page = s >> pv.pg_shift, off = s & (pg - 1);
@@ -117,8 +117,7 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(AppendParams p) {
 hipError_t launch_kv_append(const AppendParams &p, hipStream_t stream) {
   if (p.total_tokens <= 0) return hipSuccess;
   const int blocks = (p.total_tokens + kTokPerBlock - 1) / kTokPerBlock;
-  hipLaunchKernelGGL(kv_append_kernel, dim3(blocks), dim3(kThreads), 0, stream, p);
-  return hipGetLastError();
+  return launch_kernel(kv_append_kernel, dim3(blocks, p.hkv), dim3(kThreads), stream, p);
 }
 
 }  // namespace hswa

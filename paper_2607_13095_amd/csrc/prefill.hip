@@ -266,8 +266,7 @@ hipError_t launch_prefill(const PrefillParams &p, hipStream_t stream) {
   if (p.ns <= 0 || p.max_chunk_len <= 0 || p.total_tokens <= 0) return hipSuccess;
   const int npos = kRows / p.group;
   const dim3 grid((p.max_chunk_len + npos - 1) / npos, p.hkv, p.ns);
-  hipLaunchKernelGGL(prefill_kernel, grid, dim3(kThreads), 0, stream, p);
-  return hipGetLastError();
+  return launch_kernel(prefill_kernel, grid, dim3(kThreads), stream, p);
 }
 
 }  // namespace hswa

@@ -58,6 +58,11 @@ def load():
         return _lib
     if not os.path.exists(LIB_PATH):
         raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2607_13095_amd.build_lib`")
+    # torch first: its HIP runtime must be the one the library binds to, so that
+    # streams and device pointers are shared (loading the library first would
+    # bring in a second HIP runtime next to torch's own copy).
+    import torch  # noqa: F401
+
     lib = ctypes.CDLL(LIB_PATH)
     P, I32, I64, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     LP, SP, CP = _Layer, ctypes.POINTER(_Shape), ctypes.POINTER(_Cache)
