@@ -6,29 +6,50 @@
 // the block table; SWA: the ring), keys from P on come from the chunk's own
 // k_new / v_new (the chunk is appended to the cache only after this kernel).
 //
-// Work unit: one workgroup (4 waves) per (tile of 128 query rows, KV head,
-// sequence). A query row is a (position, query head) pair of the KV head's GQA
-// group, so one K/V tile in LDS serves every query head that shares it. Each
-// wave owns 32 rows (two 16-column MFMA groups). Per 64-key tile:
+// Work unit: one workgroup (8 waves, two per SIMD) per (tile of 256 query rows,
+// KV head, sequence). A query row is a (position, query head) pair of the KV
+// head's GQA group, so one K/V tile in LDS serves every query head that shares
+// it. Each wave owns 32 rows (two 16-column MFMA groups); two waves per SIMD
+// let one wave's softmax run while the other's matrix products do. Per 64-key
+// tile:
 //   S^T[key][row]  = K[key][:] . Q[row][:]          (bf16 MFMA, fp32 accumulate)
-//   online softmax per row in fp32 (exp2, scale*log2(e) folded in)
+//   online softmax per row in fp32 (exp2, scale*log2(e) folded in); the running
+//   maximum is only raised when it grows by more than 2^8, so the output rescale
+//   is rare (exact: numerator and denominator share the stale maximum)
 //   O^T[d][row]   += V^T[d][key] . P^T[key][row]    (bf16 MFMA)
-// K is staged in LDS as rows, V as its transpose, both XOR-swizzled so that the
-// 16 lanes reading one MFMA operand hit distinct banks. Keys outside the
-// workgroup's range are staged as zeros, so NaN or stale data in unused cache
-// slots never reaches an accumulator; per-element masks are applied only on
-// tiles that cross the causal diagonal, the window edge or the range ends.
+// K is staged in LDS as rows (in the order the MFMA rows consume them), V as its
+// transpose, both with padded rows so that the 16 lanes reading one operand hit
+// distinct banks; the LDS tiles are double buffered and the global loads of tile
+// j+1 are in flight while tile j computes.
+// Keys outside the workgroup's range are staged as zeros, so NaN or stale data
+// in unused cache slots never reaches an accumulator; per-element masks are
+// applied only on tiles that cross the causal diagonal, the window edge or the
+// range ends. Workgroups are mapped so that each XCD works through the query
+// tiles of a few (sequence, KV head) pairs at a time and shares their K/V in L2.
 #include "hswa_common.h"
 #include "hswa_launch.h"
 
 namespace hswa {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kRows = 128;  // query rows per workgroup
+constexpr int kThreads = 512;
+constexpr int kRows = 256;  // query rows per workgroup
 constexpr int kKT = 64;     // keys per tile
+constexpr int kCG = 2;      // 16-column MFMA groups per wave
+constexpr int kXcds = 8;
+constexpr float kRescaleLog2 = 8.f;
+// LDS rows are padded by 16 bytes, so the 16 lanes that read one MFMA operand
+// (16 consecutive LDS rows at one column) spread over all banks, and every
+// address of a wave's operand reads is a per-lane base plus a constant.
+constexpr int kKRow = kHeadDim + 8;  // K tile row (one key), in bf16 elements
+constexpr int kVRow = kKT + 8;       // V^T tile row (one dim), in bf16 elements
 
-__device__ __forceinline__ int swz_k(int key) { return (key & 3) | (((key >> 3) & 3) << 2); }
+// LDS row of key k (0..63) of a tile: the MFMA row that consumes it. Within each
+// 32-key half, keys 8a+c (c < 4) feed row 4a+c of block a (rows 0..15) and keys
+// 8a+4+c feed row 4a+c of block b (rows 16..31).
+__device__ __forceinline__ int k_lds_row(int k) {
+  return (k & 32) | ((k & 4) << 2) | ((k >> 3 & 3) << 2) | (k & 3);
+}
 
 __device__ __forceinline__ int64_t prefix_page(const PoolView &pv, int b, int key, bool &ok) {
   int lp = key >> pv.pg_shift;
@@ -42,19 +63,36 @@ __device__ __forceinline__ int64_t prefix_page(const PoolView &pv, int b, int ke
   return ok ? page : 0;
 }
 
+constexpr int kStage = kKT * kHeadDim / 8 / kThreads;  // 16-byte pieces per thread per tile (K or V)
+
+struct Stage {
+  u32x4 k[kStage], v[kStage];
+};
+
 __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
-  __shared__ __attribute__((aligned(16))) uint16_t s_k[kKT * kHeadDim];
-  __shared__ __attribute__((aligned(16))) uint16_t s_v[kHeadDim * kKT];
+  __shared__ __attribute__((aligned(16))) uint16_t s_k[2][kKT * kKRow];
+  __shared__ __attribute__((aligned(16))) uint16_t s_v[2][kHeadDim * kVRow];
 
   const PoolView &pv = p.pool;
-  const int b = blockIdx.z, g = blockIdx.y;
   const int G = p.group;
   const int npos = kRows / G;  // positions per workgroup
+
+  // XCD-aware order: workgroup ids that land on one XCD walk consecutive query
+  // tiles of the same (sequence, KV head) pair.
+  const int ntq = (p.max_chunk_len + npos - 1) / npos;
+  const int64_t total = (int64_t)ntq * p.ns * p.hkv;
+  const int64_t per_xcd = (total + kXcds - 1) / kXcds;
+  const int64_t lin = (int64_t)(blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+  if (lin >= total) return;
+  const int pair = (int)(lin / ntq);
+  const int tq = (int)(lin - (int64_t)pair * ntq);
+  const int b = pair / p.hkv, g = pair - b * p.hkv;
+
   const int tok0 = p.cu_seqlens[b];
   // never step outside q / k_new / v_new / out, whatever the device offsets say
   const int C = min(min(p.cu_seqlens[b + 1], p.total_tokens) - tok0, p.max_chunk_len);
   const int P = p.prefix_lens[b];
-  const int q0 = blockIdx.x * npos;
+  const int q0 = tq * npos;
   if (q0 >= C || P < 0 || tok0 < 0) return;
   const int q1 = min(C, q0 + npos) - 1;
   const int pfirst = P + q0, plast = P + q1;
@@ -68,14 +106,15 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   const int hkv = p.hkv, hq = p.hq;
   const int shift = pv.pg_shift, pg = 1 << shift;
   const float c2 = p.scale_log2;
+  const float thresh = kRescaleLog2 / c2;  // in raw score units
 
-  // Q^T operands and the position of each of this lane's two columns.
-  u32x4 qf[2][4];
-  int cpos[2], clo[2];
-  bool cval[2];
+  // Q^T operands and the position of each of this lane's columns.
+  u32x4 qf[kCG][4];
+  int cpos[kCG], clo[kCG];
+  bool cval[kCG];
 #pragma unroll
-  for (int cg = 0; cg < 2; ++cg) {
-    const int row = wave * 32 + cg * 16 + r;
+  for (int cg = 0; cg < kCG; ++cg) {
+    const int row = wave * (16 * kCG) + cg * 16 + r;
     const int po = row / G, head = row - po * G;
     cval[cg] = q0 + po <= q1;
     cpos[cg] = P + q0 + po;
@@ -90,18 +129,10 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
     }
   }
 
-  float m[2] = {-INFINITY, -INFINITY}, lsum[2] = {0.f, 0.f};
-  f32x4 acc[2][8];
+  // ---- staging: global -> registers -> LDS ----
+  auto load_tile = [&](int kt, Stage &st) {
 #pragma unroll
-  for (int cg = 0; cg < 2; ++cg)
-#pragma unroll
-    for (int dt = 0; dt < 8; ++dt) acc[cg][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  for (int kt = klo & ~(kKT - 1); kt <= khi; kt += kKT) {
-    __syncthreads();  // the previous tile has been consumed
-    // ---- stage K rows ----
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < kStage; ++i) {
       const int idx = tid + kThreads * i;
       const int key = idx >> 4, c = idx & 15;
       const int j = kt + key;
@@ -115,11 +146,10 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
           v = ldg128(p.k_new + ((int64_t)(tok0 + j - P) * hkv + g) * kHeadDim + c * 8);
         }
       }
-      *reinterpret_cast<u32x4 *>(s_k + key * kHeadDim + ((c ^ swz_k(key)) * 8)) = v;
+      st.k[i] = v;
     }
-    // ---- stage V^T ----
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < kStage; ++i) {
       const int idx = tid + kThreads * i;
       const int d = idx >> 3, kc = idx & 7;
       const int j0 = kt + 8 * kc;
@@ -147,107 +177,152 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
 #pragma unroll
         for (int t = 0; t < 4; ++t) v[t] = e[2 * t] | (e[2 * t + 1] << 16);
       }
-      *reinterpret_cast<u32x4 *>(s_v + d * kKT + ((kc ^ (d & 7)) * 8)) = v;
+      st.v[i] = v;
     }
-    __syncthreads();
-
-    // ---- S^T = K Q^T ----
-    float s[2][2][8];  // [half][cg][key]
+  };
+  auto store_tile = [&](int buf, const Stage &st) {
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      u32x4 ka[4], kb[4];
-      const int keya = 32 * h + 8 * (r >> 2) + (r & 3);
-      const int keyb = keya + 4;
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const int c = 4 * t + q;
-        ka[t] = *reinterpret_cast<const u32x4 *>(s_k + keya * kHeadDim + ((c ^ swz_k(keya)) * 8));
-        kb[t] = *reinterpret_cast<const u32x4 *>(s_k + keyb * kHeadDim + ((c ^ swz_k(keyb)) * 8));
-      }
-#pragma unroll
-      for (int cg = 0; cg < 2; ++cg) {
-        f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-          sa = mfma16x16x32(ka[t], qf[cg][t], sa);
-          sb = mfma16x16x32(kb[t], qf[cg][t], sb);
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          s[h][cg][i] = sa[i];
-          s[h][cg][4 + i] = sb[i];
-        }
-      }
+    for (int i = 0; i < kStage; ++i) {
+      const int idx = tid + kThreads * i;
+      const int key = idx >> 4, c = idx & 15;
+      *reinterpret_cast<u32x4 *>(&s_k[buf][k_lds_row(key) * kKRow + c * 8]) = st.k[i];
     }
+#pragma unroll
+    for (int i = 0; i < kStage; ++i) {
+      const int idx = tid + kThreads * i;
+      const int d = idx >> 3, kc = idx & 7;
+      *reinterpret_cast<u32x4 *>(&s_v[buf][d * kVRow + kc * 8]) = st.v[i];
+    }
+  };
 
-    // ---- masks (only on tiles that need them) ----
+  float m[kCG], lsum[kCG];
+  f32x4 acc[kCG][8];
+#pragma unroll
+  for (int cg = 0; cg < kCG; ++cg) {
+    m[cg] = -INFINITY;
+    lsum[cg] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) acc[cg][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  // One 64-key tile, processed as two 32-key halves (QK^T, softmax, PV each),
+  // which keeps the score and probability registers of a wave at 32 + 16.
+  auto compute_tile = [&](int buf, int kt) {
     const bool need_mask = kt + kKT - 1 > pfirst || kt < klo || kt + kKT - 1 > khi ||
                            (W > 0 && kt < plast - W + 1);
-    if (need_mask) {
-#pragma unroll
-      for (int h = 0; h < 2; ++h)
-#pragma unroll
-        for (int cg = 0; cg < 2; ++cg)
-#pragma unroll
-          for (int i = 0; i < 8; ++i) {
-            const int j = kt + 32 * h + 8 * q + i;
-            const bool ok = j <= cpos[cg] && j >= clo[cg] && j >= klo && j <= khi;
-            s[h][cg][i] = ok ? s[h][cg][i] : -INFINITY;
-          }
-    }
-
-    // ---- online softmax and O^T += V^T P^T ----
-    u32x4 pf[2][2];
-#pragma unroll
-    for (int cg = 0; cg < 2; ++cg) {
-      float cmax = -INFINITY;
-#pragma unroll
-      for (int h = 0; h < 2; ++h)
-#pragma unroll
-        for (int i = 0; i < 8; ++i) cmax = fmaxf(cmax, s[h][cg][i]);
-      cmax = wave_max_xor(cmax, 16);
-      cmax = wave_max_xor(cmax, 32);
-      const float mnew = fmaxf(m[cg], cmax);
-      const float mc = mnew == -INFINITY ? 0.f : mnew * c2;
-      const float alpha = fast_exp2(m[cg] * c2 - mc);
-      float psum = 0.f;
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        float pr[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          pr[i] = fast_exp2(fmaf(s[h][cg][i], c2, -mc));
-          psum += pr[i];
-        }
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) pf[h][cg][jj] = pack_bf16x2(pr[2 * jj], pr[2 * jj + 1]);
-      }
-      lsum[cg] = lsum[cg] * alpha + psum;
-      m[cg] = mnew;
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) acc[cg][dt] *= alpha;
-    }
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      const int kc = 4 * h + q;
+      // ---- S^T = K Q^T for keys kt + 32h .. +31 ----
+      f32x4 s[2][kCG];  // [key block a/b][column group]
+      // MFMA row r of block a is LDS row 32h + r, of block b row 32h + 16 + r
+      const uint16_t *krow = &s_k[buf][(32 * h + r) * kKRow + 8 * q];
+#pragma unroll
+      for (int cg = 0; cg < kCG; ++cg) {
+        s[0][cg] = f32x4{0.f, 0.f, 0.f, 0.f};
+        s[1][cg] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const u32x4 ka = *reinterpret_cast<const u32x4 *>(krow + 32 * t);
+        const u32x4 kb = *reinterpret_cast<const u32x4 *>(krow + 16 * kKRow + 32 * t);
+#pragma unroll
+        for (int cg = 0; cg < kCG; ++cg) {
+          s[0][cg] = mfma16x16x32(ka, qf[cg][t], s[0][cg]);
+          s[1][cg] = mfma16x16x32(kb, qf[cg][t], s[1][cg]);
+        }
+      }
+
+      // ---- masks (only on tiles that need them) ----
+      if (need_mask) {
+#pragma unroll
+        for (int ab = 0; ab < 2; ++ab)
+#pragma unroll
+          for (int cg = 0; cg < kCG; ++cg)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int j = kt + 32 * h + 8 * q + 4 * ab + i;
+              const bool ok = j <= cpos[cg] && j >= clo[cg] && j >= klo && j <= khi;
+              s[ab][cg][i] = ok ? s[ab][cg][i] : -INFINITY;
+            }
+      }
+
+      // ---- online softmax with a lazily raised maximum ----
+      float cmax[kCG];
+      bool raise = false;
+#pragma unroll
+      for (int cg = 0; cg < kCG; ++cg) {
+        float x = fmaxf(fmaxf(fmaxf(s[0][cg][0], s[0][cg][1]), fmaxf(s[0][cg][2], s[0][cg][3])),
+                        fmaxf(fmaxf(s[1][cg][0], s[1][cg][1]), fmaxf(s[1][cg][2], s[1][cg][3])));
+        x = wave_max_xor(x, 16);
+        x = wave_max_xor(x, 32);
+        cmax[cg] = x;
+        raise = raise || (x > m[cg] + thresh) || (m[cg] == -INFINITY && x > -INFINITY);
+      }
+      if (__builtin_amdgcn_ballot_w64(raise) != 0) {
+#pragma unroll
+        for (int cg = 0; cg < kCG; ++cg) {
+          const bool up = (cmax[cg] > m[cg] + thresh) || (m[cg] == -INFINITY && cmax[cg] > -INFINITY);
+          if (up) {
+            const float alpha = m[cg] == -INFINITY ? 0.f : fast_exp2((m[cg] - cmax[cg]) * c2);
+            m[cg] = cmax[cg];
+            lsum[cg] *= alpha;
+#pragma unroll
+            for (int dt = 0; dt < 8; ++dt) acc[cg][dt] *= alpha;
+          }
+        }
+      }
+      u32x4 pf[kCG];
+#pragma unroll
+      for (int cg = 0; cg < kCG; ++cg) {
+        const float mc = m[cg] == -INFINITY ? 0.f : m[cg] * c2;
+        float pr[8];
+#pragma unroll
+        for (int ab = 0; ab < 2; ++ab)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) pr[4 * ab + i] = fast_exp2(fmaf(s[ab][cg][i], c2, -mc));
+        lsum[cg] += ((pr[0] + pr[1]) + (pr[2] + pr[3])) + ((pr[4] + pr[5]) + (pr[6] + pr[7]));
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) pf[cg][jj] = pack_bf16x2(pr[2 * jj], pr[2 * jj + 1]);
+      }
+
+      // ---- O^T += V^T P^T ----
+      const uint16_t *vrow = &s_v[buf][r * kVRow + 8 * (4 * h + q)];
 #pragma unroll
       for (int dt = 0; dt < 8; ++dt) {
-        const int d = 16 * dt + r;
-        const u32x4 vf = *reinterpret_cast<const u32x4 *>(s_v + d * kKT + ((kc ^ (d & 7)) * 8));
+        const u32x4 vf = *reinterpret_cast<const u32x4 *>(vrow + 16 * dt * kVRow);
 #pragma unroll
-        for (int cg = 0; cg < 2; ++cg) acc[cg][dt] = mfma16x16x32(vf, pf[h][cg], acc[cg][dt]);
+        for (int cg = 0; cg < kCG; ++cg) acc[cg][dt] = mfma16x16x32(vf, pf[cg], acc[cg][dt]);
       }
     }
+  };
+
+  // ---- tile loop: LDS double buffer, next tile's global loads in flight ----
+  const int kt0 = klo & ~(kKT - 1);
+  const int ntiles = (khi - kt0) / kKT + 1;
+  {
+    Stage st;
+    load_tile(kt0, st);
+    store_tile(0, st);
+  }
+  __syncthreads();
+  for (int jt = 0; jt < ntiles; ++jt) {
+    const int kt = kt0 + jt * kKT;
+    const bool more = jt + 1 < ntiles;
+    Stage st;
+    if (more) load_tile(kt + kKT, st);
+    compute_tile(jt & 1, kt);
+    if (more) store_tile((jt + 1) & 1, st);
+    __syncthreads();
   }
 
   // ---- normalise and write ----
 #pragma unroll
-  for (int cg = 0; cg < 2; ++cg) {
+  for (int cg = 0; cg < kCG; ++cg) {
     float l = wave_sum_xor(lsum[cg], 16);
     l = wave_sum_xor(l, 32);
     if (!cval[cg]) continue;
     const float inv = 1.f / l;
-    const int row = wave * 32 + cg * 16 + r;
+    const int row = wave * (16 * kCG) + cg * 16 + r;
     const int po = row / G, head = row - po * G;
     uint16_t *orow = p.out + ((int64_t)(tok0 + q0 + po) * hq + (int64_t)g * G + head) * kHeadDim;
 #pragma unroll
@@ -265,8 +340,10 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
 hipError_t launch_prefill(const PrefillParams &p, hipStream_t stream) {
   if (p.ns <= 0 || p.max_chunk_len <= 0 || p.total_tokens <= 0) return hipSuccess;
   const int npos = kRows / p.group;
-  const dim3 grid((p.max_chunk_len + npos - 1) / npos, p.hkv, p.ns);
-  return launch_kernel(prefill_kernel, grid, dim3(kThreads), stream, p);
+  const int64_t ntq = (p.max_chunk_len + npos - 1) / npos;
+  const int64_t total = ntq * p.ns * p.hkv;
+  const int64_t grid = (total + kXcds - 1) / kXcds * kXcds;
+  return launch_kernel(prefill_kernel, dim3((unsigned)grid), dim3(kThreads), stream, p);
 }
 
 }  // namespace hswa
