@@ -240,11 +240,7 @@ __global__ __launch_bounds__(kWave) void decode_kernel(DecodeParams p) {
         s[i] = (keep >> i) & 1u ? sa[i] : -INFINITY;
         s[4 + i] = (keep >> (4 + i)) & 1u ? sb[i] : -INFINITY;
       }
-      float cmax = s[0];
-#pragma unroll
-      for (int i = 1; i < 8; ++i) cmax = fmaxf(cmax, s[i]);
-      cmax = wave_max_xor(cmax, 16);
-      cmax = wave_max_xor(cmax, 32);
+      const float cmax = max_xor32(max_xor16(max8(s)));
       const float mnew = fmaxf(m, cmax);
       const float mc = mnew == -INFINITY ? 0.f : mnew * c2;
       alpha = fast_exp2(m * c2 - mc);
@@ -306,8 +302,7 @@ __global__ __launch_bounds__(kWave) void decode_kernel(DecodeParams p) {
     }
 
     // Normalise and write: lane holds O^T[d = 16 dt + 4 q + i][head r].
-    lsum = wave_sum_xor(lsum, 16);
-    lsum = wave_sum_xor(lsum, 32);
+    lsum = sum_xor32(sum_xor16(lsum));
     if (r < nheads) {
       const float inv = 1.f / lsum;
       if (kSplit) {
@@ -348,7 +343,8 @@ __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(DecodeParam
   float mx = -INFINITY;
   for (int s = lane; s < nsplit; s += kWave) mx = fmaxf(mx, lse[s]);
 #pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, kWave));
+  for (int off = 8; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, kWave));
+  mx = max_xor32(max_xor16(mx));
   const float *po = p.ws_o + idx * p.max_splits * kHeadDim + 2 * lane;
   float wsum = 0.f, o0 = 0.f, o1 = 0.f;
   for (int s0 = 0; s0 < nsplit; s0 += kWave) {

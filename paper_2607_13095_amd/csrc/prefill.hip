@@ -26,6 +26,8 @@
 // applied only on tiles that cross the causal diagonal, the window edge or the
 // range ends. Workgroups are mapped so that each XCD works through the query
 // tiles of a few (sequence, KV head) pairs at a time and shares their K/V in L2.
+#include <type_traits>
+
 #include "hswa_common.h"
 #include "hswa_launch.h"
 
@@ -37,6 +39,7 @@ constexpr int kRows = 256;  // query rows per workgroup
 constexpr int kKT = 64;     // keys per tile
 constexpr int kCG = 2;      // 16-column MFMA groups per wave
 constexpr int kXcds = 8;
+constexpr int kBufs = 3;  // LDS tile buffers (the pipeline reads two tiles while a third is written)
 constexpr float kRescaleLog2 = 8.f;
 // LDS rows are padded by 16 bytes, so the 16 lanes that read one MFMA operand
 // (16 consecutive LDS rows at one column) spread over all banks, and every
@@ -70,8 +73,8 @@ struct Stage {
 };
 
 __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
-  __shared__ __attribute__((aligned(16))) uint16_t s_k[2][kKT * kKRow];
-  __shared__ __attribute__((aligned(16))) uint16_t s_v[2][kHeadDim * kVRow];
+  __shared__ __attribute__((aligned(16))) uint16_t s_k[kBufs][kKT * kKRow];
+  __shared__ __attribute__((aligned(16))) uint16_t s_v[kBufs][kHeadDim * kVRow];
 
   const PoolView &pv = p.pool;
   const int G = p.group;
@@ -180,6 +183,20 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
       st.v[i] = v;
     }
   };
+  // Interior tile: every key cached, in range and (PG >= 64) on one page whose
+  // id was fetched ahead; plain 16-byte loads at computed offsets.
+  auto load_tile_page = [&](int kt, int page, Stage &st) {
+    const int64_t pg64 = max(page, 0);
+    const int off = kt & (pg - 1);
+    const uint16_t *kbase = pv.k_pool + ((((pg64 * hkv + g) << shift) + off) * kHeadDim);
+    const uint16_t *vbase = pv.v_pool + ((((pg64 * hkv + g) * kHeadDim) << shift) + off);
+#pragma unroll
+    for (int i = 0; i < kStage; ++i) {
+      const int idx = tid + kThreads * i;
+      st.k[i] = ldg128(kbase + (idx >> 4) * kHeadDim + (idx & 15) * 8);
+      st.v[i] = ldg128(vbase + ((idx >> 3) << shift) + (idx & 7) * 8);
+    }
+  };
   auto store_tile = [&](int buf, const Stage &st) {
 #pragma unroll
     for (int i = 0; i < kStage; ++i) {
@@ -207,119 +224,184 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
 
   // One 64-key tile, processed as two 32-key halves (QK^T, softmax, PV each),
   // which keeps the score and probability registers of a wave at 32 + 16.
-  auto compute_tile = [&](int buf, int kt) {
-    const bool need_mask = kt + kKT - 1 > pfirst || kt < klo || kt + kKT - 1 > khi ||
-                           (W > 0 && kt < plast - W + 1);
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      // ---- S^T = K Q^T for keys kt + 32h .. +31 ----
-      f32x4 s[2][kCG];  // [key block a/b][column group]
-      // MFMA row r of block a is LDS row 32h + r, of block b row 32h + 16 + r
-      const uint16_t *krow = &s_k[buf][(32 * h + r) * kKRow + 8 * q];
-#pragma unroll
-      for (int cg = 0; cg < kCG; ++cg) {
-        s[0][cg] = f32x4{0.f, 0.f, 0.f, 0.f};
-        s[1][cg] = f32x4{0.f, 0.f, 0.f, 0.f};
-      }
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const u32x4 ka = *reinterpret_cast<const u32x4 *>(krow + 32 * t);
-        const u32x4 kb = *reinterpret_cast<const u32x4 *>(krow + 16 * kKRow + 32 * t);
-#pragma unroll
-        for (int cg = 0; cg < kCG; ++cg) {
-          s[0][cg] = mfma16x16x32(ka, qf[cg][t], s[0][cg]);
-          s[1][cg] = mfma16x16x32(kb, qf[cg][t], s[1][cg]);
+  // ---- pipelined tile loop ----
+  // Work is split into half tiles of 32 keys. The QK^T of the next half is
+  // issued before the softmax of the current one, so the matrix cores and the
+  // VALU work of a wave can overlap; LDS holds three tiles (the two being read
+  // and the one being written), with one barrier per tile.
+  const int kt0 = klo & ~(kKT - 1);
+  const int ntiles = (khi - kt0) / kKT + 1;
+  const bool page_tiles = shift >= 6;
+  // A tile is "interior" when all of its keys are cached, inside [klo, khi]
+  // and (PG >= 64) on a single page; its page id is looked up one tile ahead.
+  auto interior = [&](int kt) { return page_tiles && kt >= klo && kt + kKT - 1 <= khi && kt + kKT - 1 < P; };
+  // Page ids of interior tiles come from a per-wave window of the block table:
+  // lane i holds the physical page of logical page tab_lp0 + i, refilled every
+  // 64 pages, and a tile's id is read with v_readlane (no per-tile memory
+  // round trip). -1 marks a tile that is not interior or whose page is invalid.
+  int tab_page = -1, tab_lp0 = -(1 << 30);
+  auto tile_page = [&](int kt) {
+    if (!interior(kt)) return -1;
+    const int lp = kt >> shift;
+    if (lp - tab_lp0 >= kWave || lp < tab_lp0) {
+      tab_lp0 = lp;
+      const int lpl = lp + lane;
+      int page = -1;
+      if (lpl <= ((P - 1) >> shift)) {
+        const int e = pv.ring > 0 ? lpl % pv.ring : lpl;
+        if (e < pv.stride) {
+          const int64_t v = pv.table[(int64_t)b * pv.stride + e];
+          page = (v >= 0 && v < pv.num_pages) ? (int)v : -1;
         }
       }
+      tab_page = page;
+    }
+    return __builtin_amdgcn_readlane(tab_page, lp - tab_lp0);
+  };
+  auto fetch = [&](int kt, int page, Stage &st) {
+    if (page >= 0) load_tile_page(kt, page, st);
+    else load_tile(kt, st);
+  };
 
-      // ---- masks (only on tiles that need them) ----
-      if (need_mask) {
+  // QK^T of one half tile: S^T for keys kt + 32h .. +31.
+  auto qk_half = [&](int buf, int h, f32x4 (&sc)[2][kCG]) {
+    // MFMA row r of block a is LDS row 32h + r, of block b row 32h + 16 + r
+    const uint16_t *krow = &s_k[buf][(32 * h + r) * kKRow + 8 * q];
 #pragma unroll
-        for (int ab = 0; ab < 2; ++ab)
+    for (int cg = 0; cg < kCG; ++cg) {
+      sc[0][cg] = f32x4{0.f, 0.f, 0.f, 0.f};
+      sc[1][cg] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
 #pragma unroll
-          for (int cg = 0; cg < kCG; ++cg)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const int j = kt + 32 * h + 8 * q + 4 * ab + i;
-              const bool ok = j <= cpos[cg] && j >= clo[cg] && j >= klo && j <= khi;
-              s[ab][cg][i] = ok ? s[ab][cg][i] : -INFINITY;
-            }
-      }
-
-      // ---- online softmax with a lazily raised maximum ----
-      float cmax[kCG];
-      bool raise = false;
+    for (int t = 0; t < 4; ++t) {
+      const u32x4 ka = *reinterpret_cast<const u32x4 *>(krow + 32 * t);
+      const u32x4 kb = *reinterpret_cast<const u32x4 *>(krow + 16 * kKRow + 32 * t);
 #pragma unroll
       for (int cg = 0; cg < kCG; ++cg) {
-        float x = fmaxf(fmaxf(fmaxf(s[0][cg][0], s[0][cg][1]), fmaxf(s[0][cg][2], s[0][cg][3])),
-                        fmaxf(fmaxf(s[1][cg][0], s[1][cg][1]), fmaxf(s[1][cg][2], s[1][cg][3])));
-        x = wave_max_xor(x, 16);
-        x = wave_max_xor(x, 32);
-        cmax[cg] = x;
-        raise = raise || (x > m[cg] + thresh) || (m[cg] == -INFINITY && x > -INFINITY);
-      }
-      if (__builtin_amdgcn_ballot_w64(raise) != 0) {
-#pragma unroll
-        for (int cg = 0; cg < kCG; ++cg) {
-          const bool up = (cmax[cg] > m[cg] + thresh) || (m[cg] == -INFINITY && cmax[cg] > -INFINITY);
-          if (up) {
-            const float alpha = m[cg] == -INFINITY ? 0.f : fast_exp2((m[cg] - cmax[cg]) * c2);
-            m[cg] = cmax[cg];
-            lsum[cg] *= alpha;
-#pragma unroll
-            for (int dt = 0; dt < 8; ++dt) acc[cg][dt] *= alpha;
-          }
-        }
-      }
-      u32x4 pf[kCG];
-#pragma unroll
-      for (int cg = 0; cg < kCG; ++cg) {
-        const float mc = m[cg] == -INFINITY ? 0.f : m[cg] * c2;
-        float pr[8];
-#pragma unroll
-        for (int ab = 0; ab < 2; ++ab)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) pr[4 * ab + i] = fast_exp2(fmaf(s[ab][cg][i], c2, -mc));
-        lsum[cg] += ((pr[0] + pr[1]) + (pr[2] + pr[3])) + ((pr[4] + pr[5]) + (pr[6] + pr[7]));
-#pragma unroll
-        for (int jj = 0; jj < 4; ++jj) pf[cg][jj] = pack_bf16x2(pr[2 * jj], pr[2 * jj + 1]);
-      }
-
-      // ---- O^T += V^T P^T ----
-      const uint16_t *vrow = &s_v[buf][r * kVRow + 8 * (4 * h + q)];
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) {
-        const u32x4 vf = *reinterpret_cast<const u32x4 *>(vrow + 16 * dt * kVRow);
-#pragma unroll
-        for (int cg = 0; cg < kCG; ++cg) acc[cg][dt] = mfma16x16x32(vf, pf[cg], acc[cg][dt]);
+        sc[0][cg] = mfma16x16x32(ka, qf[cg][t], sc[0][cg]);
+        sc[1][cg] = mfma16x16x32(kb, qf[cg][t], sc[1][cg]);
       }
     }
   };
+  // Per-element mask of a half tile on the diagonal, window edge or range ends.
+  auto mask_half = [&](int kt, int h, f32x4 (&sc)[2][kCG]) {
+    // this lane's 8 keys are kt + 32h + 8q + e, e = 4 ab + i; allowed e form
+    // the interval [lo_e, hi_e] of the column's visible keys
+    const int j0 = kt + 32 * h + 8 * q;
+#pragma unroll
+    for (int cg = 0; cg < kCG; ++cg) {
+      const int lo_e = max(max(clo[cg], klo) - j0, 0);
+      const int hi_e = min(min(cpos[cg], khi) - j0, 7);
+      const uint32_t bits = hi_e < lo_e ? 0u : ((2u << hi_e) - 1u) & ~((1u << lo_e) - 1u);
+#pragma unroll
+      for (int ab = 0; ab < 2; ++ab)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) sc[ab][cg][i] = (bits >> (4 * ab + i)) & 1u ? sc[ab][cg][i] : -INFINITY;
+    }
+  };
+  auto needs_mask = [&](int kt) {
+    return kt + kKT - 1 > pfirst || kt < klo || kt + kKT - 1 > khi || (W > 0 && kt < plast - W + 1);
+  };
+  // Row maximum, lazy raise of the running maximum (rare rescale of the
+  // output), then exp2 and the bf16 P^T operand; the row sums use the same
+  // bf16-rounded probabilities as the PV product.
+  auto softmax_max = [&](f32x4 (&sc)[2][kCG]) {
+    float cmax[kCG];
+    bool raise = false;
+#pragma unroll
+    for (int cg = 0; cg < kCG; ++cg) {
+      const float v8[8] = {sc[0][cg][0], sc[0][cg][1], sc[0][cg][2], sc[0][cg][3],
+                           sc[1][cg][0], sc[1][cg][1], sc[1][cg][2], sc[1][cg][3]};
+      cmax[cg] = max_xor32(max_xor16(max8(v8)));
+      raise = raise || (cmax[cg] > m[cg] + thresh) || (m[cg] == -INFINITY && cmax[cg] > -INFINITY);
+    }
+    if (__builtin_amdgcn_ballot_w64(raise) != 0) {
+#pragma unroll
+      for (int cg = 0; cg < kCG; ++cg) {
+        const bool up = (cmax[cg] > m[cg] + thresh) || (m[cg] == -INFINITY && cmax[cg] > -INFINITY);
+        if (up) {
+          const float alpha = m[cg] == -INFINITY ? 0.f : fast_exp2((m[cg] - cmax[cg]) * c2);
+          m[cg] = cmax[cg];
+          lsum[cg] *= alpha;
+#pragma unroll
+          for (int dt = 0; dt < 8; ++dt) acc[cg][dt] *= alpha;
+        }
+      }
+    }
+  };
+  auto softmax_exp = [&](f32x4 (&sc)[2][kCG], u32x4 (&pf)[kCG]) {
+#pragma unroll
+    for (int cg = 0; cg < kCG; ++cg) {
+      const float mc = m[cg] == -INFINITY ? 0.f : m[cg] * c2;
+      float pr[8];
+#pragma unroll
+      for (int ab = 0; ab < 2; ++ab)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) pr[4 * ab + i] = fast_exp2(fmaf(sc[ab][cg][i], c2, -mc));
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) pf[cg][jj] = pack_bf16x2(pr[2 * jj], pr[2 * jj + 1]);
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) lsum[cg] = dot2_bf16_ones(pf[cg][jj], lsum[cg]);
+    }
+  };
+  // O^T += V^T P^T for one half tile.
+  auto pv_half = [&](int buf, int h, const u32x4 (&pf)[kCG]) {
+    const uint16_t *vrow = &s_v[buf][r * kVRow + 8 * (4 * h + q)];
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) {
+      const u32x4 vf = *reinterpret_cast<const u32x4 *>(vrow + 16 * dt * kVRow);
+#pragma unroll
+      for (int cg = 0; cg < kCG; ++cg) acc[cg][dt] = mfma16x16x32(vf, pf[cg], acc[cg][dt]);
+    }
+  };
 
-  // ---- tile loop: LDS double buffer, next tile's global loads in flight ----
-  const int kt0 = klo & ~(kKT - 1);
-  const int ntiles = (khi - kt0) / kKT + 1;
-  {
-    Stage st;
-    load_tile(kt0, st);
-    store_tile(0, st);
+  // Prologue: tiles 0 and 1 in LDS, tile 2's loads in flight, QK^T of (0, 0).
+  Stage st;
+  fetch(kt0, tile_page(kt0), st);
+  store_tile(0, st);
+  if (ntiles > 1) {
+    fetch(kt0 + kKT, tile_page(kt0 + kKT), st);
+    store_tile(1, st);
   }
+  if (ntiles > 2) fetch(kt0 + 2 * kKT, tile_page(kt0 + 2 * kKT), st);
   __syncthreads();
+  f32x4 s_a[2][kCG], s_b[2][kCG];
+  qk_half(0, 0, s_a);
+
   for (int jt = 0; jt < ntiles; ++jt) {
     const int kt = kt0 + jt * kKT;
-    const bool more = jt + 1 < ntiles;
-    Stage st;
-    if (more) load_tile(kt + kKT, st);
-    compute_tile(jt & 1, kt);
-    if (more) store_tile((jt + 1) & 1, st);
+    const int buf = jt % kBufs;
+    const bool masked = needs_mask(kt);
+    // [B] softmax of (jt, 0) with the QK^T of (jt, 1) issued alongside
+    if (masked) mask_half(kt, 0, s_a);
+    softmax_max(s_a);
+    {
+      u32x4 pf[kCG];
+      qk_half(buf, 1, s_b);
+      softmax_exp(s_a, pf);
+      // [C] PV of (jt, 0)
+      pv_half(buf, 0, pf);
+    }
+    // every wave is past its PV of tile jt-1: tile jt+2 may overwrite it
     __syncthreads();
+    if (jt + 2 < ntiles) store_tile((jt + 2) % kBufs, st);
+    if (jt + 3 < ntiles) fetch(kt + 3 * kKT, tile_page(kt + 3 * kKT), st);
+    // [D] softmax of (jt, 1) with the QK^T of (jt + 1, 0) issued alongside
+    if (masked) mask_half(kt, 1, s_b);
+    softmax_max(s_b);
+    {
+      u32x4 pf[kCG];
+      if (jt + 1 < ntiles) qk_half((jt + 1) % kBufs, 0, s_a);
+      softmax_exp(s_b, pf);
+      // [E] PV of (jt, 1)
+      pv_half(buf, 1, pf);
+    }
   }
 
   // ---- normalise and write ----
 #pragma unroll
   for (int cg = 0; cg < kCG; ++cg) {
-    float l = wave_sum_xor(lsum[cg], 16);
-    l = wave_sum_xor(l, 32);
+    const float l = sum_xor32(sum_xor16(lsum[cg]));
     if (!cval[cg]) continue;
     const float inv = 1.f / l;
     const int row = wave * (16 * kCG) + cg * 16 + r;
