@@ -14,8 +14,9 @@
 // tile:
 //   S^T[key][row]  = K[key][:] . Q[row][:]          (bf16 MFMA, fp32 accumulate)
 //   online softmax per row in fp32 (exp2, scale*log2(e) folded in); the running
-//   maximum is only raised when it grows by more than 2^8, so the output rescale
-//   is rare (exact: numerator and denominator share the stale maximum)
+//   maximum is only raised when a score exceeds it by more than 2^8 in exp2
+//   units, so the output rescale is rare (exact: numerator and denominator share
+//   the stale maximum)
 //   O^T[d][row]   += V^T[d][key] . P^T[key][row]    (bf16 MFMA)
 // K is staged in LDS as rows (in the order the MFMA rows consume them), V as its
 // transpose, both with padded rows so that the 16 lanes reading one operand hit
@@ -26,6 +27,7 @@
 // applied only on tiles that cross the causal diagonal, the window edge or the
 // range ends. Workgroups are mapped so that each XCD works through the query
 // tiles of a few (sequence, KV head) pairs at a time and shares their K/V in L2.
+#include <cfloat>
 #include <type_traits>
 
 #include "hswa_common.h"
@@ -216,7 +218,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   f32x4 acc[kCG][8];
 #pragma unroll
   for (int cg = 0; cg < kCG; ++cg) {
-    m[cg] = -INFINITY;
+    m[cg] = -FLT_MAX;
     lsum[cg] = 0.f;
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) acc[cg][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -302,37 +304,42 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   auto needs_mask = [&](int kt) {
     return kt + kKT - 1 > pfirst || kt < klo || kt + kKT - 1 > khi || (W > 0 && kt < plast - W + 1);
   };
-  // Row maximum, lazy raise of the running maximum (rare rescale of the
-  // output), then exp2 and the bf16 P^T operand; the row sums use the same
-  // bf16-rounded probabilities as the PV product.
+  // Lazy raise of the running maximum. Each lane compares the maximum of its
+  // own 8 scores with m + thresh; only if some lane exceeds it (a ballot) is
+  // the exact column maximum formed across the 4 lanes that share a column
+  // and the output rescaled. Otherwise every probability stays below 2^8.
+  // The running maximum starts at -FLT_MAX, a finite value: exp2 of a masked
+  // score (-inf) is then 0 with no NaN from (-inf) - (-inf), and the first
+  // finite score always raises it (alpha = exp2(-huge) = 0).
   auto softmax_max = [&](f32x4 (&sc)[2][kCG]) {
-    float cmax[kCG];
+    float lmax[kCG];
     bool raise = false;
 #pragma unroll
     for (int cg = 0; cg < kCG; ++cg) {
       const float v8[8] = {sc[0][cg][0], sc[0][cg][1], sc[0][cg][2], sc[0][cg][3],
                            sc[1][cg][0], sc[1][cg][1], sc[1][cg][2], sc[1][cg][3]};
-      cmax[cg] = max_xor32(max_xor16(max8(v8)));
-      raise = raise || (cmax[cg] > m[cg] + thresh) || (m[cg] == -INFINITY && cmax[cg] > -INFINITY);
+      lmax[cg] = max8(v8);
+      raise = raise || lmax[cg] > m[cg] + thresh;
     }
     if (__builtin_amdgcn_ballot_w64(raise) != 0) {
 #pragma unroll
       for (int cg = 0; cg < kCG; ++cg) {
-        const bool up = (cmax[cg] > m[cg] + thresh) || (m[cg] == -INFINITY && cmax[cg] > -INFINITY);
-        if (up) {
-          const float alpha = m[cg] == -INFINITY ? 0.f : fast_exp2((m[cg] - cmax[cg]) * c2);
-          m[cg] = cmax[cg];
-          lsum[cg] *= alpha;
+        const float cmax = max_xor32(max_xor16(lmax[cg]));
+        const bool up = cmax > m[cg] + thresh;
+        const float alpha = up ? fast_exp2((m[cg] - cmax) * c2) : 1.f;
+        m[cg] = up ? cmax : m[cg];
+        lsum[cg] *= alpha;
 #pragma unroll
-          for (int dt = 0; dt < 8; ++dt) acc[cg][dt] *= alpha;
-        }
+        for (int dt = 0; dt < 8; ++dt) acc[cg][dt] *= alpha;
       }
     }
   };
+  // exp2 and the bf16 P^T operand; the row sums use the same bf16-rounded
+  // probabilities as the PV product.
   auto softmax_exp = [&](f32x4 (&sc)[2][kCG], u32x4 (&pf)[kCG]) {
 #pragma unroll
     for (int cg = 0; cg < kCG; ++cg) {
-      const float mc = m[cg] == -INFINITY ? 0.f : m[cg] * c2;
+      const float mc = m[cg] * c2;
       float pr[8];
 #pragma unroll
       for (int ab = 0; ab < 2; ++ab)
