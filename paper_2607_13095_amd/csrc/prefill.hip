@@ -398,7 +398,9 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
     softmax_max(s_b);
     {
       u32x4 pf[kCG];
-      if (jt + 1 < ntiles) qk_half((jt + 1) % kBufs, 0, s_a);
+      // unconditional, so that it interleaves with the exponentials; after the
+      // last tile it reads a stale buffer and the result is never used
+      qk_half((jt + 1) % kBufs, 0, s_a);
       softmax_exp(s_b, pf);
       // [E] PV of (jt, 1)
       pv_half(buf, 1, pf);
