@@ -38,6 +38,39 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2516.6
 
+# Bytes moved between L2 and memory per call, from rocprofv3 --pmc FETCH_SIZE and
+# --pmc WRITE_SIZE runs of this script with --copy-calibration, each counter
+# scaled by what it reads for the plain 1 GiB copy (FETCH_SIZE reads 524,300 KiB
+# for 1 GiB read: x2.0; WRITE_SIZE reads 1,048,576 KiB for 1 GiB written: x1.0).
+# A figure holds only for the kernel sources it was taken on (SHA-256 below);
+# once they change the benchmark reports null until it is measured again.
+MEASURED_TRAFFIC = {
+    "decode_full": {"sources": ["decode.hip", "hswa_common.h", "hswa_launch.h"],
+                    "sha256": "0ffd4cc00447e707213add8c8522450de6be58a37f473ad40737a523d049b5da",
+                    "fetch_bytes": 5174920806, "write_bytes": 67424870},
+    "prefill_full": {"sources": ["prefill.hip", "hswa_common.h", "hswa_launch.h"],
+                     "sha256": "2c72fa0a413dcdef9ea799b187ad8cf339d13000e9eca866e3d5862d05956c8c",
+                     "fetch_bytes": 1217915051, "write_bytes": 134217728},
+}
+
+
+def sources_sha256(names):
+    import hashlib
+
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2607_13095_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(key):
+    """HBM-side bytes per call of a kernel, or None if its sources changed."""
+    t = MEASURED_TRAFFIC[key]
+    if sources_sha256(t["sources"]) != t["sha256"]:
+        return None
+    return int(t["fetch_bytes"] + t["write_bytes"])
+
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
@@ -51,7 +84,28 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prefill", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target oracle time for the CPU baseline")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="first run a plain 1 GiB device copy three times (reference for HBM byte counters)")
     return ap.parse_args()
+
+
+COPY_BYTES = 1 << 30
+
+
+def copy_calibration():
+    """A plain device-to-device copy of COPY_BYTES, three times: under
+    rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE its readings give the factor that
+    turns the counters into bytes."""
+    import torch
+
+    src = torch.ones(COPY_BYTES // 2, dtype=torch.bfloat16, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    log(f"[bench] copy calibration: 3 x {COPY_BYTES} bytes copied")
+    del src, dst
+    torch.cuda.empty_cache()
 
 
 # ----------------------------------------------------------------------------
@@ -251,7 +305,7 @@ class PrefillBench:
         hswa.prefill(L["layer"], self.shape, L["kv"].cache, L["q"], L["kn"], L["vn"], self.cu, self.pre, self.maxc,
                      L["out"])
 
-    def time_kind(self, kind, reps=10, warmup=2):
+    def time_kind(self, kind, reps=20, warmup=10):
         import torch
 
         L = next(x for x in self.layers if x["kind"] == kind)
@@ -281,6 +335,8 @@ def main():
 
     hswa.load()
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        copy_calibration()
 
     wl = synth.decode_b64()
     log(f"[bench] setting up {wl.name}")
@@ -323,7 +379,9 @@ def main():
             "swa_ms": round(s_ms, 4), "swa_gbs": round(s_gbs, 1), "swa_frac_hbm": round(s_gbs / HBM_PEAK_GBS, 4),
             "swa_tflops": round(pb.flops["swa"] / (s_ms * 1e-3) / 1e12, 2),
             "roofline": {"bound": "mfma", "achieved": round(f_tf, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
-                         "unit": "TFLOP/s", "frac": round(f_tf / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None},
+                         "unit": "TFLOP/s", "frac": round(f_tf / MFMA_BF16_PEAK_TFLOPS, 4),
+                         "traffic": measured_traffic("prefill_full"), "algorithmic_bytes": pb.bytes["full"],
+                         "algorithmic_flops": pb.flops["full"]},
         }
         log(f"[bench] prefill FULL {f_ms:.3f} ms = {f_tf:.1f} TFLOP/s; SWA {s_ms:.3f} ms = {s_gbs:.0f} GB/s")
         del pb
@@ -353,8 +411,9 @@ def main():
                    "decode_bytes": dec_bytes, "full_decode_ms": round(full_avg, 5),
                    "swa_decode_ms": round(swa_ms, 5)},
         "roofline": {"bound": "hbm", "achieved": round(full_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(full_gbs / HBM_PEAK_GBS, 4), "traffic": None,
-                     "kernel": "FULL-layer decode (split-KV + merge)"},
+                     "frac": round(full_gbs / HBM_PEAK_GBS, 4), "traffic": measured_traffic("decode_full"),
+                     "algorithmic_bytes": db.bytes["full"],
+                     "kernel": "FULL-layer decode call: decode_kernel<true,true> + decode_merge_kernel"},
         "prefill": prefill,
         "cpu_baseline": cpu,
     }
