@@ -35,9 +35,12 @@
  *   softmax and accumulation are fp32; outputs are rounded to bf16 with
  *   round-to-nearest-even.
  * Layout. Per layer there is one K pool and one V pool of `num_pages` pages:
- *     K pool: bf16 [num_pages][Hkv][page_size][head_dim]  (a row per token)
- *     V pool: bf16 [num_pages][Hkv][head_dim][page_size]  (transposed page)
- *   Slot s addresses page s / page_size at in-page offset s % page_size.
+ *     K pool: bf16 [num_pages][Hkv][page_size][head_dim]      (a row per token)
+ *     V pool: bf16 [num_pages][Hkv][page_size/VB][head_dim][VB], VB = min(page_size, 32)
+ *             (the keys of a page in blocks of VB, each block transposed, so
+ *             the V^T of 32 consecutive keys of one head is one 8 KiB run)
+ *   Slot s addresses page s / page_size at in-page offset o = s % page_size;
+ *   its V values sit in block o / VB, column o % VB.
  *   Every pool offset is computed in 64-bit.
  * Block tables (int32, device, row stride `table_stride`):
  *     FULL layer: table[b][i] = physical page of logical page i (positions
@@ -103,7 +106,7 @@ typedef struct {
 /* One layer's pool pair and its block table (see Layout / Block tables). */
 typedef struct {
   void *k_pool;               /* device, bf16 [num_pages][Hkv][PG][D]          */
-  void *v_pool;               /* device, bf16 [num_pages][Hkv][D][PG]          */
+  void *v_pool;               /* device, bf16 [num_pages][Hkv][PG/VB][D][VB]   */
   int64_t num_pages;
   const int32_t *block_table; /* device, int32 [ns][table_stride]              */
   int32_t table_stride;

@@ -20,9 +20,11 @@ Readings where the paper is silent:
     by sequence: table[b][i] = perm[offset_b + i] for i < n_b, -1 elsewhere,
     with n_b = ceil(L_b_final / PG) for FULL and n_b = R for SWA.
 
-Pool layout (one pool per layer and per K / V):
-  K pool: [num_pages][Hkv][PG][D]  (key-major rows inside a page)
-  V pool: [num_pages][Hkv][D][PG]  (transposed inside a page)
+Pool layout (one pool per layer and per K / V; the paper fixes none, this is
+the library's own):
+  K pool: [num_pages][Hkv][PG][D]          (key-major rows inside a page)
+  V pool: [num_pages][Hkv][PG/VB][D][VB]   (blocks of VB = min(PG, 32) keys,
+                                             each transposed)
 A slot s addresses page s // PG, in-page offset s % PG.
 """
 
@@ -99,18 +101,23 @@ def slot_mapping(kind, window, page_size, table, start_pos, new_lens) -> np.ndar
 def apply_append(k_pool, v_pool, slots, k_new, v_new):
     """Expected pool content after an append (copies; bf16 bits as uint16).
 
-    k_pool: [P][Hkv][PG][D], v_pool: [P][Hkv][D][PG]; k_new, v_new: [T][Hkv][D].
-    Tokens whose slot is -1 are not stored.
+    k_pool: [P][Hkv][PG][D] (one row per slot). v_pool: [P][Hkv][PG/VB][D][VB]:
+    the keys of a page in blocks of VB = min(PG, 32), each block stored with
+    the dim index outer. k_new, v_new: [T][Hkv][D]. Tokens whose slot is -1 are
+    not stored.
     """
     k_pool = np.array(k_pool, copy=True)
     v_pool = np.array(v_pool, copy=True)
     pg = k_pool.shape[2]
+    vb = v_pool.shape[4]
+    if vb != min(pg, 32) or v_pool.shape[2] * vb != pg:
+        raise ValueError("v_pool blocks must hold min(PG, 32) keys")
     for t, s in enumerate(np.asarray(slots)):
         if s < 0:
             continue
         page, off = int(s) // pg, int(s) % pg
         k_pool[page, :, off, :] = k_new[t]
-        v_pool[page, :, :, off] = v_new[t]
+        v_pool[page, :, off // vb, :, off % vb] = v_new[t]
     return k_pool, v_pool
 
 

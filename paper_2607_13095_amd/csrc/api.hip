@@ -62,6 +62,7 @@ hswa_status make_pool(hswa_layer layer, const hswa_shape *sh, const hswa_cache *
   pv.table = cache->block_table;
   pv.stride = cache->table_stride;
   pv.pg_shift = log2_exact(sh->page_size);
+  pv.vb_shift = pv.pg_shift < hswa::kVBlockShiftMax ? pv.pg_shift : hswa::kVBlockShiftMax;
   if (layer.kind == HSWA_LAYER_SWA) {
     pv.ring = hswa_ring_pages(layer.window, sh->page_size);
     pv.window = layer.window;

@@ -14,7 +14,7 @@
 // Per item the wave walks 32-key chunks and runs both products on the bf16
 // matrix cores with the GQA query heads as the 16 MFMA columns:
 //   S^T[key][head]  = K[key][:] . Q[head][:]        (K rows straight from HBM)
-//   O^T[d][head]   += V^T[d][key] . P^T[key][head]   (V pages are stored [D][PG])
+//   O^T[d][head]   += V^T[d][key] . P^T[key][head]   (V pages hold [D][32] blocks)
 // The 32 keys of a chunk are assigned to MFMA rows so that the score tile comes
 // out with each lane holding 8 consecutive keys of one head, which is exactly
 // the lane layout the PV product needs for P^T: no shuffle between the two.
@@ -75,8 +75,10 @@ __global__ __launch_bounds__(kWave) void decode_kernel(DecodeParams p) {
   // (used when a 32-key chunk never straddles two pages, i.e. PG >= 32).
   const uint32_t koff_a = ((8 * (r >> 2) + (r & 3)) * kHeadDim + 8 * q) * 2;
   const uint32_t koff_b = koff_a + 4 * kHeadDim * 2;
-  const uint32_t voff = ((uint32_t)r << shift) * 2 + 16 * q;
-  const uint32_t vstep = (16u << shift) * 2;  // 16 dims of V^T
+  // V^T of a 32-key chunk is one [D][32] block when PG >= 32: lane reads dims
+  // 16 dt + r, keys 8 q .. 8 q + 7 of it.
+  const uint32_t voff = (r * 32 + 8 * q) * 2;
+  const uint32_t vstep = 16 * 32 * 2;  // 16 dims of a V block
 
   // Which item this workgroup runs. Split items are numbered over the pieces
   // that exist (sequence by sequence, piece by piece, head group fastest), so
@@ -183,8 +185,10 @@ __global__ __launch_bounds__(kWave) void decode_kernel(DecodeParams p) {
     auto issue_v = [&](int c, int page, Chunk &ch) {
       const int cbase = cfirst + c * kChunk;
       const int64_t pg64 = max(page, 0);
+      // PG >= 32 here, so VB = 32: the chunk is block (cbase mod PG) / 32 of the page-head
       const char *vbase = reinterpret_cast<const char *>(pv.v_pool) +
-                          ((((pg64 * hkv + g) * kHeadDim) << shift) + (cbase & (pg - 1))) * 2;
+                          ((((pg64 * hkv + g) << shift) << kHeadDimShift) +
+                           ((int64_t)((cbase & (pg - 1)) >> 5) << (5 + kHeadDimShift))) * 2;
       ch.kv0 = cbase + 8 * q;
       ch.vok = page >= 0;
 #pragma unroll
@@ -209,14 +213,14 @@ __global__ __launch_bounds__(kWave) void decode_kernel(DecodeParams p) {
       const int64_t pa64 = max(pa, 0), pb64 = max(pb, 0), pv64 = max(pvv, 0);
       const uint16_t *krow_a = pv.k_pool + (((pa64 * hkv + g) << shift) + (ka & (pg - 1))) * kHeadDim;
       const uint16_t *krow_b = pv.k_pool + (((pb64 * hkv + g) << shift) + (kb2 & (pg - 1))) * kHeadDim;
-      const uint16_t *vcol = pv.v_pool + ((pv64 * hkv + g) * kHeadDim << shift) + (kvg & (pg - 1));
+      const uint16_t *vcol = pv.v_pool + v_offset(pv, pv64, hkv, g, kvg & (pg - 1), r);
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         ch.ka[t] = ldg128(krow_a + 32 * t + 8 * q);
         ch.kb[t] = ldg128(krow_b + 32 * t + 8 * q);
       }
 #pragma unroll
-      for (int dt = 0; dt < 8; ++dt) ch.v[dt] = ldg128(vcol + ((int64_t)(16 * dt + r) << shift));
+      for (int dt = 0; dt < 8; ++dt) ch.v[dt] = ldg128(vcol + ((int64_t)(16 * dt) << pv.vb_shift));
     };
 
     // QK^T and the online softmax of one chunk: returns P^T packed as bf16 and

@@ -31,6 +31,13 @@ __device__ __forceinline__ u32x4 ldg128(const void *p) {
 
 __device__ __forceinline__ void stg128(void *p, u32x4 v) { *reinterpret_cast<u32x4 *>(p) = v; }
 
+// Element offset in the V pool of (page, KV head g, in-page key offset o, dim d).
+__device__ __forceinline__ int64_t v_offset(const PoolView &pv, int64_t page, int hkv, int g, int o, int d) {
+  const int vb = pv.vb_shift;
+  return (((page * hkv + g) << pv.pg_shift) << kHeadDimShift) + ((int64_t)(o >> vb) << (vb + kHeadDimShift)) +
+         ((int64_t)d << vb) + (o & ((1 << vb) - 1));
+}
+
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 

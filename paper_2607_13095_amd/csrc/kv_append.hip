@@ -7,9 +7,10 @@
 //
 // One workgroup handles 8 consecutive tokens of the flattened batch for one KV
 // head. The K row of a token is one contiguous 256-byte run per KV head in the
-// pool; V pages are stored transposed ([D][PG] per head), so 8 tokens that land
-// on 8 consecutive, 8-aligned slots of one page are written as one 16-byte
-// store per dim; anything else falls back to 2-byte stores.
+// pool; V pages are stored as transposed blocks of VB = min(PG, 32) keys
+// ([D][VB] per block and head), so 8 tokens that land on 8 consecutive,
+// 8-aligned slots of one page are written as one 16-byte store per dim;
+// anything else falls back to 2-byte stores.
 #include "hswa_common.h"
 #include "hswa_launch.h"
 
@@ -98,7 +99,7 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(AppendParams p) {
         const uint32_t hi = src[(int64_t)(2 * k + 1) * hkv * kHeadDim];
         w[k] = lo | (hi << 16);
       }
-      stg128(pv.v_pool + ((page * hkv + g) * kHeadDim + d) * pg + off, w);
+      stg128(pv.v_pool + v_offset(pv, page, hkv, g, (int)off, d), w);
     }
   } else {
     for (int i = tid; i < ntok * kHeadDim; i += kThreads) {
@@ -106,8 +107,7 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(AppendParams p) {
       const int64_t s = s_slot[tok];
       if (s < 0) continue;
       const int64_t page = s >> pv.pg_shift, off = s & (pg - 1);
-      pv.v_pool[((page * hkv + g) * kHeadDim + d) * pg + off] =
-          p.v_new[((int64_t)(t0 + tok) * hkv + g) * kHeadDim + d];
+      pv.v_pool[v_offset(pv, page, hkv, g, (int)off, d)] = p.v_new[((int64_t)(t0 + tok) * hkv + g) * kHeadDim + d];
     }
   }
 }

@@ -69,6 +69,13 @@ __device__ __forceinline__ int64_t prefix_page(const PoolView &pv, int b, int ke
 }
 
 constexpr int kStage = kKT * kHeadDim / 8 / kThreads;  // 16-byte pieces per thread per tile (K or V)
+static_assert(kStage == 2 && kKT == 64, "V staging maps piece i of a thread to 32-key block i");
+
+// V^T tile staging: piece i of thread tid holds dim tid / 4 and keys
+// 8 * (4 i + tid % 4) .. +7 of the tile, which in the pool is the 16 bytes at
+// element 8 * tid of the tile's 32-key block i.
+__device__ __forceinline__ int v_piece_dim(int tid) { return tid >> 2; }
+__device__ __forceinline__ int v_piece_keys(int tid, int i) { return 4 * i + (tid & 3); }
 
 struct Stage {
   u32x4 k[kStage], v[kStage];
@@ -155,14 +162,13 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
     }
 #pragma unroll
     for (int i = 0; i < kStage; ++i) {
-      const int idx = tid + kThreads * i;
-      const int d = idx >> 3, kc = idx & 7;
+      const int d = v_piece_dim(tid), kc = v_piece_keys(tid, i);
       const int j0 = kt + 8 * kc;
       u32x4 v = {0u, 0u, 0u, 0u};
       if (j0 >= klo && j0 + 7 <= khi && j0 + 7 < P) {
         bool ok;
         const int64_t page = prefix_page(pv, b, j0, ok);
-        if (ok) v = ldg128(pv.v_pool + ((page * hkv + g) * kHeadDim + d) * pg + (j0 & (pg - 1)));
+        if (ok) v = ldg128(pv.v_pool + v_offset(pv, page, hkv, g, j0 & (pg - 1), d));
       } else if (j0 + 7 >= klo && j0 <= khi) {
         uint32_t e[8];
 #pragma unroll
@@ -173,7 +179,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
             if (j < P) {
               bool ok;
               const int64_t page = prefix_page(pv, b, j, ok);
-              if (ok) e[t] = pv.v_pool[((page * hkv + g) * kHeadDim + d) * pg + (j & (pg - 1))];
+              if (ok) e[t] = pv.v_pool[v_offset(pv, page, hkv, g, j & (pg - 1), d)];
             } else {
               e[t] = p.v_new[((int64_t)(tok0 + j - P) * hkv + g) * kHeadDim + d];
             }
@@ -186,17 +192,19 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
     }
   };
   // Interior tile: every key cached, in range and (PG >= 64) on one page whose
-  // id was fetched ahead; plain 16-byte loads at computed offsets.
+  // id was fetched ahead; the K tile is 16 KiB and the V tile two [D][32]
+  // blocks of 8 KiB, all contiguous: plain 16-byte loads, consecutive threads
+  // at consecutive addresses.
   auto load_tile_page = [&](int kt, int page, Stage &st) {
     const int64_t pg64 = max(page, 0);
     const int off = kt & (pg - 1);
     const uint16_t *kbase = pv.k_pool + ((((pg64 * hkv + g) << shift) + off) * kHeadDim);
-    const uint16_t *vbase = pv.v_pool + ((((pg64 * hkv + g) * kHeadDim) << shift) + off);
+    const uint16_t *vbase = pv.v_pool + v_offset(pv, pg64, hkv, g, off, 0);
 #pragma unroll
     for (int i = 0; i < kStage; ++i) {
       const int idx = tid + kThreads * i;
       st.k[i] = ldg128(kbase + (idx >> 4) * kHeadDim + (idx & 15) * 8);
-      st.v[i] = ldg128(vbase + ((idx >> 3) << shift) + (idx & 7) * 8);
+      st.v[i] = ldg128(vbase + i * (32 * kHeadDim) + tid * 8);
     }
   };
   auto store_tile = [&](int buf, const Stage &st) {
@@ -207,11 +215,8 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
       *reinterpret_cast<u32x4 *>(&s_k[buf][k_lds_row(key) * kKRow + c * 8]) = st.k[i];
     }
 #pragma unroll
-    for (int i = 0; i < kStage; ++i) {
-      const int idx = tid + kThreads * i;
-      const int d = idx >> 3, kc = idx & 7;
-      *reinterpret_cast<u32x4 *>(&s_v[buf][d * kVRow + kc * 8]) = st.v[i];
-    }
+    for (int i = 0; i < kStage; ++i)
+      *reinterpret_cast<u32x4 *>(&s_v[buf][v_piece_dim(tid) * kVRow + v_piece_keys(tid, i) * 8]) = st.v[i];
   };
 
   float m[kCG], lsum[kCG];

@@ -148,19 +148,32 @@ def _i32():
     return (torch.int32,)
 
 
+V_BLOCK_MAX = 32
+
+
+def v_block(page_size: int) -> int:
+    """Keys per transposed V block: VB = min(PG, 32)."""
+    return min(int(page_size), V_BLOCK_MAX)
+
+
+def v_pool_shape(num_pages: int, num_kv_heads: int, page_size: int, head_dim: int = 128):
+    vb = v_block(page_size)
+    return (int(num_pages), int(num_kv_heads), int(page_size) // vb, int(head_dim), vb)
+
+
 class Cache:
     """One layer's K pool, V pool and block table (device tensors).
 
-    k_pool: bf16 [num_pages, Hkv, PG, D]; v_pool: bf16 [num_pages, Hkv, D, PG];
-    block_table: int32 [ns, stride].
+    k_pool: bf16 [num_pages, Hkv, PG, D]; v_pool: bf16 [num_pages, Hkv, PG/VB, D, VB]
+    with VB = min(PG, 32) (see include/hswa.h); block_table: int32 [ns, stride].
     """
 
     def __init__(self, k_pool, v_pool, block_table):
-        if k_pool.dim() != 4 or v_pool.dim() != 4 or block_table.dim() != 2:
-            raise ValueError("pools are 4-D, the block table is 2-D")
+        if k_pool.dim() != 4 or v_pool.dim() != 5 or block_table.dim() != 2:
+            raise ValueError("k_pool is 4-D, v_pool 5-D, the block table 2-D")
         npg, hkv, pg, d = k_pool.shape
-        if tuple(v_pool.shape) != (npg, hkv, d, pg):
-            raise ValueError("v_pool must be [num_pages, Hkv, D, PG]")
+        if tuple(v_pool.shape) != v_pool_shape(npg, hkv, pg, d):
+            raise ValueError("v_pool must be [num_pages, Hkv, PG/VB, D, VB] with VB = min(PG, 32)")
         self.k_pool, self.v_pool, self.block_table = k_pool, v_pool, block_table
         self.num_pages, self.stride = int(npg), int(block_table.shape[1])
 

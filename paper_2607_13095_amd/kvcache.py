@@ -40,7 +40,8 @@ class LayerKV:
         self.table_host = hswa.build_block_table(layer, pg, final_lens, perm, stride)
         self.block_table = torch.from_numpy(self.table_host).to(device)
         self.k_pool = torch.full((self.num_pages, hkv, pg, d), fill, dtype=torch.bfloat16, device=device)
-        self.v_pool = torch.full((self.num_pages, hkv, d, pg), fill, dtype=torch.bfloat16, device=device)
+        self.v_pool = torch.full(hswa.v_pool_shape(self.num_pages, hkv, pg, d), fill, dtype=torch.bfloat16,
+                                 device=device)
         self.cache = hswa.Cache(self.k_pool, self.v_pool, self.block_table)
 
     def nbytes(self) -> int:

@@ -73,7 +73,8 @@ def test_poisoned_stale_ring_slots(gpu_lib):
             if pos < L - window:  # held by the ring but outside the window of the query at L-1
                 page = int(kv.table_host[b][entry])
                 kv.k_pool[page, :, off, :] = float("nan")
-                kv.v_pool[page, :, :, off] = float("nan")
+                vb = hswa.v_block(pg)
+                kv.v_pool[page, :, off // vb, :, off % vb] = float("nan")
                 poisoned += 1
     assert poisoned > 0
     out2 = torch.empty_like(out1)

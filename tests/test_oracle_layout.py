@@ -61,14 +61,31 @@ def test_slot_mapping_full_hand_worked():
 def test_apply_append_hand_worked():
     pg, hkv, d = 2, 1, 3
     kp = np.zeros((2, hkv, pg, d), dtype=np.uint16)
-    vp = np.zeros((2, hkv, d, pg), dtype=np.uint16)
+    vp = np.zeros((2, hkv, 1, d, pg), dtype=np.uint16)  # one block of VB = PG = 2 keys
     kn = np.array([[[1, 2, 3]], [[4, 5, 6]], [[7, 8, 9]]], dtype=np.uint16)
     vn = kn + 100
     k2, v2 = Lo.apply_append(kp, vp, [3, -1, 0], kn, vn)
     # slot 3 = page 1, offset 1; slot 0 = page 0, offset 0; token 1 dropped
     assert k2[1, 0, 1].tolist() == [1, 2, 3] and k2[0, 0, 0].tolist() == [7, 8, 9]
-    assert v2[1, 0, :, 1].tolist() == [101, 102, 103] and v2[0, 0, :, 0].tolist() == [107, 108, 109]
+    assert v2[1, 0, 0, :, 1].tolist() == [101, 102, 103] and v2[0, 0, 0, :, 0].tolist() == [107, 108, 109]
     assert int(k2.sum()) == 1 + 2 + 3 + 7 + 8 + 9
+
+
+def test_apply_append_v_blocks_hand_worked():
+    """PG = 64: V is stored in two blocks of 32 keys; in-page offset 40 is key 8
+    of block 1, so its dims sit at flat element 1*32*D + d*32 + 8 of the page."""
+    pg, hkv, d = 64, 2, 4
+    kp = np.zeros((3, hkv, pg, d), dtype=np.uint16)
+    vp = np.zeros((3, hkv, 2, d, 32), dtype=np.uint16)
+    kn = np.arange(1, 1 + hkv * d, dtype=np.uint16).reshape(1, hkv, d)
+    _, v2 = Lo.apply_append(kp, vp, [2 * 64 + 40], kn, kn + 50)
+    flat = v2.reshape(3, hkv, pg * d)
+    for g in range(hkv):
+        for dd in range(d):
+            assert flat[2, g, 32 * d + dd * 32 + 8] == kn[0, g, dd] + 50
+    assert int((v2 != 0).sum()) == hkv * d
+    with pytest.raises(ValueError):
+        Lo.apply_append(kp, np.zeros((3, hkv, d, pg), dtype=np.uint16)[..., None], [0], kn, kn)
 
 
 @pytest.mark.parametrize("window,pg", [(4, 2), (128, 16), (128, 64), (1, 16), (129, 64), (5, 4)])
