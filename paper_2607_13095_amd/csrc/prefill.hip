@@ -20,8 +20,8 @@
 //   O^T[d][row]   += V^T[d][key] . P^T[key][row]    (bf16 MFMA)
 // K is staged in LDS as rows (in the order the MFMA rows consume them), V as its
 // transpose, both with padded rows so that the 16 lanes reading one operand hit
-// distinct banks; the LDS tiles are double buffered and the global loads of tile
-// j+1 are in flight while tile j computes.
+// distinct banks; four LDS tile buffers let tile j+3 be stored while tiles j and
+// j+1 are read, and the global loads of tile j+4 are in flight meanwhile.
 // Keys outside the workgroup's range are staged as zeros, so NaN or stale data
 // in unused cache slots never reaches an accumulator; per-element masks are
 // applied only on tiles that cross the causal diagonal, the window edge or the
@@ -41,7 +41,7 @@ constexpr int kRows = 256;  // query rows per workgroup
 constexpr int kKT = 64;     // keys per tile
 constexpr int kCG = 2;      // 16-column MFMA groups per wave
 constexpr int kXcds = 8;
-constexpr int kBufs = 3;  // LDS tile buffers (the pipeline reads two tiles while a third is written)
+constexpr int kBufs = 4;  // LDS tile buffers: two being read, one written, one spare
 constexpr float kRescaleLog2 = 8.f;
 // LDS rows are padded by 16 bytes, so the 16 lanes that read one MFMA operand
 // (16 consecutive LDS rows at one column) spread over all banks, and every
@@ -367,7 +367,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
     }
   };
 
-  // Prologue: tiles 0 and 1 in LDS, tile 2's loads in flight, QK^T of (0, 0).
+  // Prologue: tiles 0..2 in LDS, tile 3's loads in flight, QK^T of (0, 0).
   Stage st;
   fetch(kt0, tile_page(kt0), st);
   store_tile(0, st);
@@ -375,7 +375,11 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
     fetch(kt0 + kKT, tile_page(kt0 + kKT), st);
     store_tile(1, st);
   }
-  if (ntiles > 2) fetch(kt0 + 2 * kKT, tile_page(kt0 + 2 * kKT), st);
+  if (ntiles > 2) {
+    fetch(kt0 + 2 * kKT, tile_page(kt0 + 2 * kKT), st);
+    store_tile(2, st);
+  }
+  if (ntiles > 3) fetch(kt0 + 3 * kKT, tile_page(kt0 + 3 * kKT), st);
   __syncthreads();
   f32x4 s_a[2][kCG], s_b[2][kCG];
   qk_half(0, 0, s_a);
@@ -384,32 +388,28 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
     const int kt = kt0 + jt * kKT;
     const int buf = jt % kBufs;
     const bool masked = needs_mask(kt);
-    // [B] softmax of (jt, 0) with the QK^T of (jt, 1) issued alongside
+    u32x4 pf[kCG];
+    // softmax of (jt, 0) with the QK^T of (jt, 1) issued alongside, PV of (jt, 0)
     if (masked) mask_half(kt, 0, s_a);
     softmax_max(s_a);
-    {
-      u32x4 pf[kCG];
-      qk_half(buf, 1, s_b);
-      softmax_exp(s_a, pf);
-      // [C] PV of (jt, 0)
-      pv_half(buf, 0, pf);
-    }
-    // every wave is past its PV of tile jt-1: tile jt+2 may overwrite it
+    qk_half(buf, 1, s_b);
+    softmax_exp(s_a, pf);
+    pv_half(buf, 0, pf);
+    // Every wave is past its last read of tile jt-1: tile jt+3 (in registers
+    // since the previous iteration) overwrites its buffer, and tile jt+4's
+    // loads go out, a whole iteration ahead of their store.
     __syncthreads();
-    if (jt + 2 < ntiles) store_tile((jt + 2) % kBufs, st);
-    if (jt + 3 < ntiles) fetch(kt + 3 * kKT, tile_page(kt + 3 * kKT), st);
-    // [D] softmax of (jt, 1) with the QK^T of (jt + 1, 0) issued alongside
+    if (jt + 3 < ntiles) store_tile((jt + 3) % kBufs, st);
+    if (jt + 4 < ntiles) fetch(kt + 4 * kKT, tile_page(kt + 4 * kKT), st);
+    // softmax of (jt, 1) with the QK^T of (jt + 1, 0) issued alongside (it is
+    // unconditional so that it interleaves with the exponentials; after the
+    // last tile it reads a stale buffer and the result is never used), PV of
+    // (jt, 1)
     if (masked) mask_half(kt, 1, s_b);
     softmax_max(s_b);
-    {
-      u32x4 pf[kCG];
-      // unconditional, so that it interleaves with the exponentials; after the
-      // last tile it reads a stale buffer and the result is never used
-      qk_half((jt + 1) % kBufs, 0, s_a);
-      softmax_exp(s_b, pf);
-      // [E] PV of (jt, 1)
-      pv_half(buf, 1, pf);
-    }
+    qk_half((jt + 1) % kBufs, 0, s_a);
+    softmax_exp(s_b, pf);
+    pv_half(buf, 1, pf);
   }
 
   // ---- normalise and write ----
