@@ -68,6 +68,8 @@ __device__ __forceinline__ int64_t prefix_page(const PoolView &pv, int b, int ke
   return ok ? page : 0;
 }
 
+constexpr int kKTileBytes = kKT * kKRow * 2;
+constexpr int kBufBytes = kKTileBytes + kHeadDim * kVRow * 2;
 constexpr int kStage = kKT * kHeadDim / 8 / kThreads;  // 16-byte pieces per thread per tile (K or V)
 static_assert(kStage == 2 && kKT == 64, "V staging maps piece i of a thread to 32-key block i");
 
@@ -82,8 +84,8 @@ struct Stage {
 };
 
 __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
-  __shared__ __attribute__((aligned(16))) uint16_t s_k[kBufs][kKT * kKRow];
-  __shared__ __attribute__((aligned(16))) uint16_t s_v[kBufs][kHeadDim * kVRow];
+  // kBufs tile buffers, each a K tile then a V^T tile (byte offsets below)
+  __shared__ __attribute__((aligned(16))) unsigned char s_lds[kBufs * kBufBytes];
 
   const PoolView &pv = p.pool;
   const int G = p.group;
@@ -207,16 +209,21 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
       st.v[i] = ldg128(vbase + i * (32 * kHeadDim) + tid * 8);
     }
   };
+  // LDS addresses are a per-lane byte offset (fixed for the kernel) plus the
+  // buffer's byte offset (a scalar), with everything else in the instruction's
+  // immediate offset field.
+  auto buf_off = [&](int buf) { return (uint32_t)__builtin_amdgcn_readfirstlane(buf * kBufBytes); };
+  auto lds128 = [&](uint32_t off) { return reinterpret_cast<u32x4 *>(s_lds + off); };
+  const uint32_t st_k0 = (k_lds_row(tid >> 4) * kKRow + (tid & 15) * 8) * 2;  // piece 0; piece 1 is 32 rows on
+  const uint32_t st_v0 = kKTileBytes + (v_piece_dim(tid) * kVRow + v_piece_keys(tid, 0) * 8) * 2;
   auto store_tile = [&](int buf, const Stage &st) {
-#pragma unroll
-    for (int i = 0; i < kStage; ++i) {
-      const int idx = tid + kThreads * i;
-      const int key = idx >> 4, c = idx & 15;
-      *reinterpret_cast<u32x4 *>(&s_k[buf][k_lds_row(key) * kKRow + c * 8]) = st.k[i];
-    }
-#pragma unroll
-    for (int i = 0; i < kStage; ++i)
-      *reinterpret_cast<u32x4 *>(&s_v[buf][v_piece_dim(tid) * kVRow + v_piece_keys(tid, i) * 8]) = st.v[i];
+    static_assert(kStage == 2, "two pieces per thread");
+    const uint32_t bo = buf_off(buf);
+    // piece 1 of K is key + 32 (LDS row + 32), of V keys + 32 (block 1)
+    *lds128(bo + st_k0) = st.k[0];
+    *lds128(bo + st_k0 + 32 * kKRow * 2) = st.k[1];
+    *lds128(bo + st_v0) = st.v[0];
+    *lds128(bo + st_v0 + 32 * 2) = st.v[1];
   };
 
   float m[kCG], lsum[kCG];
@@ -271,9 +278,11 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   };
 
   // QK^T of one half tile: S^T for keys kt + 32h .. +31.
+  const uint32_t qk_lane = (r * kKRow + 8 * q) * 2;
+  const uint32_t pv_lane = kKTileBytes + (r * kVRow + 8 * q) * 2;
   auto qk_half = [&](int buf, int h, f32x4 (&sc)[2][kCG]) {
     // MFMA row r of block a is LDS row 32h + r, of block b row 32h + 16 + r
-    const uint16_t *krow = &s_k[buf][(32 * h + r) * kKRow + 8 * q];
+    const uint32_t a = buf_off(buf) + qk_lane + 32 * h * kKRow * 2;
 #pragma unroll
     for (int cg = 0; cg < kCG; ++cg) {
       sc[0][cg] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -281,8 +290,8 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
     }
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      const u32x4 ka = *reinterpret_cast<const u32x4 *>(krow + 32 * t);
-      const u32x4 kb = *reinterpret_cast<const u32x4 *>(krow + 16 * kKRow + 32 * t);
+      const u32x4 ka = *lds128(a + 64 * t);
+      const u32x4 kb = *lds128(a + 16 * kKRow * 2 + 64 * t);
 #pragma unroll
       for (int cg = 0; cg < kCG; ++cg) {
         sc[0][cg] = mfma16x16x32(ka, qf[cg][t], sc[0][cg]);
@@ -358,10 +367,10 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   };
   // O^T += V^T P^T for one half tile.
   auto pv_half = [&](int buf, int h, const u32x4 (&pf)[kCG]) {
-    const uint16_t *vrow = &s_v[buf][r * kVRow + 8 * (4 * h + q)];
+    const uint32_t a = buf_off(buf) + pv_lane + 64 * h;  // keys 32h + 8q .. +7
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) {
-      const u32x4 vf = *reinterpret_cast<const u32x4 *>(vrow + 16 * dt * kVRow);
+      const u32x4 vf = *lds128(a + 16 * dt * kVRow * 2);
 #pragma unroll
       for (int cg = 0; cg < kCG; ++cg) acc[cg][dt] = mfma16x16x32(vf, pf[cg], acc[cg][dt]);
     }
