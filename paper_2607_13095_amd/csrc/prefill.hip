@@ -366,14 +366,16 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
     }
   };
   // O^T += V^T P^T for one half tile.
-  auto pv_half = [&](int buf, int h, const u32x4 (&pf)[kCG]) {
+  auto load_v = [&](int buf, int h, u32x4 (&vf)[8]) {
     const uint32_t a = buf_off(buf) + pv_lane + 64 * h;  // keys 32h + 8q .. +7
 #pragma unroll
-    for (int dt = 0; dt < 8; ++dt) {
-      const u32x4 vf = *lds128(a + 16 * dt * kVRow * 2);
+    for (int dt = 0; dt < 8; ++dt) vf[dt] = *lds128(a + 16 * dt * kVRow * 2);
+  };
+  auto pv_ops = [&](const u32x4 (&vf)[8], const u32x4 (&pf)[kCG]) {
 #pragma unroll
-      for (int cg = 0; cg < kCG; ++cg) acc[cg][dt] = mfma16x16x32(vf, pf[cg], acc[cg][dt]);
-    }
+    for (int dt = 0; dt < 8; ++dt)
+#pragma unroll
+      for (int cg = 0; cg < kCG; ++cg) acc[cg][dt] = mfma16x16x32(vf[dt], pf[cg], acc[cg][dt]);
   };
 
   // Prologue: tiles 0..2 in LDS, tile 3's loads in flight, QK^T of (0, 0).
@@ -397,13 +399,14 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
     const int kt = kt0 + jt * kKT;
     const int buf = jt % kBufs;
     const bool masked = needs_mask(kt);
-    u32x4 pf[kCG];
+    u32x4 pf[kCG], vf[8];
     // softmax of (jt, 0) with the QK^T of (jt, 1) issued alongside, PV of (jt, 0)
+    load_v(buf, 0, vf);
     if (masked) mask_half(kt, 0, s_a);
     softmax_max(s_a);
     qk_half(buf, 1, s_b);
     softmax_exp(s_a, pf);
-    pv_half(buf, 0, pf);
+    pv_ops(vf, pf);
     // Every wave is past its last read of tile jt-1: tile jt+3 (in registers
     // since the previous iteration) overwrites its buffer, and tile jt+4's
     // loads go out, a whole iteration ahead of their store.
@@ -414,11 +417,12 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
     // unconditional so that it interleaves with the exponentials; after the
     // last tile it reads a stale buffer and the result is never used), PV of
     // (jt, 1)
+    load_v(buf, 1, vf);
     if (masked) mask_half(kt, 1, s_b);
     softmax_max(s_b);
     qk_half((jt + 1) % kBufs, 0, s_a);
     softmax_exp(s_b, pf);
-    pv_half(buf, 1, pf);
+    pv_ops(vf, pf);
   }
 
   // ---- normalise and write ----
