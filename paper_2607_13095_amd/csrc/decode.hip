@@ -355,12 +355,21 @@ __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(DecodeParam
     const int s = s0 + lane;
     const float w = s < nsplit ? fast_exp2(lse[s] - mx) : 0.f;
     const int n = min(kWave, nsplit - s0);
-    for (int k = 0; k < n; ++k) {
-      const float wk = __shfl(w, k, kWave);
-      const float2 v = *reinterpret_cast<const float2 *>(po + (int64_t)(s0 + k) * kHeadDim);
-      wsum += wk;
-      o0 = fmaf(wk, v.x, o0);
-      o1 = fmaf(wk, v.y, o1);
+    // 8 pieces per step: their loads are independent and go out together
+    for (int k0 = 0; k0 < n; k0 += 8) {
+      float2 v[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        v[k] = k0 + k < n ? *reinterpret_cast<const float2 *>(po + (int64_t)(s0 + k0 + k) * kHeadDim)
+                          : float2{0.f, 0.f};
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const float wk = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, w), min(k0 + k, kWave - 1)));
+        const float wkk = k0 + k < n ? wk : 0.f;
+        wsum += wkk;
+        o0 = fmaf(wkk, v[k].x, o0);
+        o1 = fmaf(wkk, v[k].y, o1);
+      }
     }
   }
   const float inv = 1.f / wsum;
