@@ -46,11 +46,11 @@ MFMA_BF16_PEAK_TFLOPS = 2516.6
 # once they change the benchmark reports null until it is measured again.
 MEASURED_TRAFFIC = {
     "decode_full": {"sources": ["decode.hip", "hswa_common.h", "hswa_launch.h"],
-                    "sha256": "0ffd4cc00447e707213add8c8522450de6be58a37f473ad40737a523d049b5da",
-                    "fetch_bytes": 5174920806, "write_bytes": 67424870},
+                    "sha256": "087fae7adfe6543279d19194bb2934fa52a3f34e9e0844e22133539a4ec6c223",
+                    "fetch_bytes": 4134086042, "write_bytes": 66944614},
     "prefill_full": {"sources": ["prefill.hip", "hswa_common.h", "hswa_launch.h"],
-                     "sha256": "2c72fa0a413dcdef9ea799b187ad8cf339d13000e9eca866e3d5862d05956c8c",
-                     "fetch_bytes": 1217915051, "write_bytes": 134217728},
+                     "sha256": "2fadac2ca521139209ee458bdfce1828168cd33e2bedfeb2c51c72e9559e4da4",
+                     "fetch_bytes": 1491017664, "write_bytes": 134217728},
 }
 
 
