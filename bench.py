@@ -322,6 +322,71 @@ class PrefillBench:
         return float(np.median(ts))
 
 
+def allocator_report(wl, reps=20):
+    """SWA layer of the decode workload over explicit-release tables from the
+    dual-pool allocator (HSWA_LAYER_SWA_PAGED): pages held per sequence, host
+    cost of one decode step's allocator calls, and the decode call's time."""
+    import time
+
+    import torch
+
+    import synth
+    from paper_2607_13095_amd import hswa
+
+    hq, hkv, d, pg, W = wl.hq, wl.hkv, wl.head_dim, wl.page_size, wl.window
+    ns = wl.ns
+    ctx = np.asarray(wl.prefix, dtype=np.int64)
+    stride = int(-(-(int(ctx.max()) + 2) // pg))
+    swa_pages = ns * (-(-(W + 1) // pg) + 2)
+    alloc = hswa.Allocator(pg, W, ns * stride, swa_pages, ns, stride, 1)
+    shape = hswa.Shape(hq, hkv, d, pg)
+    layer = hswa.Layer.swa_paged(W)
+    for b in range(ns):
+        assert alloc.admit(b, int(ctx[b]), 1) == 0 and alloc.extend(b, int(ctx[b])) == 0
+    _, swa_tab = alloc.tables()
+    kp = torch.full((swa_pages, hkv, pg, d), float("nan"), dtype=torch.bfloat16, device="cuda")
+    vp = torch.full(hswa.v_pool_shape(swa_pages, hkv, pg, d), float("nan"), dtype=torch.bfloat16, device="cuda")
+    cache = hswa.Cache(kp, vp, torch.from_numpy(swa_tab).cuda())
+    i32 = lambda x: torch.as_tensor(np.asarray(x, dtype=np.int32), device="cuda")  # noqa: E731
+    # the last W positions of every sequence (earlier ones are not held and would be dropped)
+    lo = np.maximum(ctx - W, 0)
+    n = ctx - lo
+    kh = synth.torch_normal_bf16((int(n.sum()), hkv, d), "cuda", wl.seed, 9, 0, synth.TAG_K)
+    vh = synth.torch_normal_bf16((int(n.sum()), hkv, d), "cuda", wl.seed, 9, 0, synth.TAG_V)
+    hswa.kv_append(layer, shape, cache, kh, vh, i32(synth.cu_seqlens(n)), i32(lo))
+    # one decode step: host allocator calls, then append + decode on the GPU
+    t0 = time.perf_counter()
+    for b in range(ns):
+        assert alloc.extend(b, int(ctx[b]) + 1) == 0
+    _, swa_tab = alloc.tables()
+    for b in range(ns):
+        alloc.step_end(b, True)
+    host_us = (time.perf_counter() - t0) * 1e6
+    cache = hswa.Cache(kp, vp, torch.from_numpy(swa_tab).cuda())
+    kn = synth.torch_normal_bf16((ns, hkv, d), "cuda", wl.seed, 9, 0, synth.TAG_KDEC)
+    q = synth.torch_normal_bf16((ns, hq, d), "cuda", wl.seed, 9, 0, synth.TAG_QDEC)
+    hswa.kv_append(layer, shape, cache, kn, kn, i32(np.arange(ns + 1)), i32(ctx))
+    out = torch.empty((ns, hq, d), dtype=torch.bfloat16, device="cuda")
+    lens, maxc = i32(ctx + 1), int(ctx.max()) + 1
+    for _ in range(3):
+        hswa.decode(layer, shape, cache, q, lens, maxc, out)
+    ts = []
+    for _ in range(reps):
+        a, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        hswa.decode(layer, shape, cache, q, lens, maxc, out)
+        b_.record()
+        b_.synchronize()
+        ts.append(a.elapsed_time(b_))
+    per_seq = [alloc.usage(b)[1] for b in range(ns)]
+    full_used = alloc.usage(-1)[0]
+    alloc.close()
+    return {"layer": "SWA over explicit-release tables", "swa_paged_decode_ms": round(float(np.median(ts)), 5),
+            "swa_pages_per_seq": [int(min(per_seq)), int(max(per_seq))],
+            "swa_pages_per_seq_bound": int(-(-(W - 1) // pg) + 1),
+            "full_pages_held": int(full_used), "host_us_per_decode_step": round(host_us, 1)}
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -387,6 +452,10 @@ def main():
         del pb
         torch.cuda.empty_cache()
 
+    log("[bench] explicit-release allocator")
+    alloc_rep = allocator_report(wl)
+    log(f"[bench] allocator: {alloc_rep}")
+
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] CPU baseline (oracle)")
@@ -415,6 +484,7 @@ def main():
                      "algorithmic_bytes": db.bytes["full"],
                      "kernel": "FULL-layer decode call: decode_kernel<true,true> + decode_merge_kernel"},
         "prefill": prefill,
+        "allocator": alloc_rep,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

@@ -83,11 +83,19 @@ typedef enum {
 } hswa_status;
 
 /* Layer kind flag ("Compute Analysis": SWA layers attend within a local
- * window, FULL layers attend globally). */
-typedef enum { HSWA_LAYER_FULL = 0, HSWA_LAYER_SWA = 1 } hswa_layer_kind;
+ * window, FULL layers attend globally).
+ *   HSWA_LAYER_SWA:       SWA layer over a per-sequence ring of pages (see
+ *                         Block tables): a fixed O(W) set of pages per sequence.
+ *   HSWA_LAYER_SWA_PAGED: SWA layer over a block table indexed like a FULL
+ *                         layer's (logical page -> SWA page), in which pages
+ *                         outside the window have been released (-1): the
+ *                         explicit-release form of the SWA pool, whose tables
+ *                         come from hswa_allocator below. Tokens appended to a
+ *                         -1 entry are not stored (slot -1). */
+typedef enum { HSWA_LAYER_FULL = 0, HSWA_LAYER_SWA = 1, HSWA_LAYER_SWA_PAGED = 2 } hswa_layer_kind;
 
-/* kind: hswa_layer_kind. window: W >= 1 for SWA (counts the query itself);
- * ignored for FULL. */
+/* kind: hswa_layer_kind. window: W >= 1 for SWA and SWA_PAGED (counts the
+ * query itself); ignored for FULL. */
 typedef struct {
   int32_t kind;
   int32_t window;
@@ -201,6 +209,70 @@ hswa_status hswa_decode(hswa_layer layer, const hswa_shape *shape, const hswa_ca
 
 /* Static string naming a status. */
 const char *hswa_status_string(hswa_status status);
+
+/* ---- explicit-release dual-pool page allocator (host) -------------------
+ * "KVCache Dual-Pool Design": separate FULL and SWA pools with their own
+ * capacities; admission checks both; the FULL index (logical page i of a
+ * sequence = positions i*PG .. i*PG+PG-1) is authoritative and the SWA table
+ * maps the same logical pages to SWA pages. "SWA-Aware Prefix Cache Tree":
+ * out-of-window SWA pages are released at the end of every prefill chunk,
+ * every N decode steps and at request end, so SWA usage per sequence stays at
+ * window (or chunk) size. The tables are the block tables of a FULL layer and
+ * of an HSWA_LAYER_SWA_PAGED layer.
+ * An allocator is a host object owned by the caller (create / destroy); it
+ * touches no device memory. Calls on one allocator must not overlap; distinct
+ * allocators are independent. Physical pages are handed out from per-pool
+ * free stacks (initially in increasing order); a call that fails changes
+ * nothing. */
+typedef struct hswa_allocator hswa_allocator;
+
+typedef struct {
+  int32_t page_size;     /* tokens per page, both pools (>= 1)                  */
+  int32_t window;        /* W >= 1                                             */
+  int64_t full_pages;    /* FULL pool capacity in pages                        */
+  int64_t swa_pages;     /* SWA pool capacity in pages                         */
+  int32_t max_seqs;      /* sequence slots 0 .. max_seqs-1 (table rows)        */
+  int32_t table_stride;  /* logical pages per table row (max length / PG)      */
+  int32_t release_every; /* N >= 1: decode steps between out-of-window releases */
+} hswa_allocator_config;
+
+hswa_status hswa_allocator_create(const hswa_allocator_config *config, hswa_allocator **out);
+void hswa_allocator_destroy(hswa_allocator *alloc);
+
+/* Admission of a request into the free slot `seq`: succeeds only if both pools
+ * can hold it now (FULL: ceil(len / PG) pages; SWA: ceil(min(len, W+chunk) /
+ * PG) + 1 pages, the window plus one chunk of `chunk` tokens). Reserves
+ * nothing; the sequence starts empty. HSWA_ERR_CAPACITY if a pool (or the
+ * table stride) is short, HSWA_ERR_INVALID_ARG if the slot is in use. */
+hswa_status hswa_allocator_admit(hswa_allocator *alloc, int32_t seq, int64_t len, int32_t chunk);
+
+/* Grow sequence `seq` to new_len tokens before the prefill / append of
+ * positions [len, new_len): FULL pages for every new logical page; SWA pages
+ * for the positions in [max(len, new_len - W), new_len) that are not held yet
+ * (the window of the query at new_len - 1, which a decode step reads back from
+ * the pool, and of the next one; earlier new positions are read from the pool
+ * by no query and are not stored). All or nothing: HSWA_ERR_CAPACITY if a pool
+ * or the stride is short. */
+hswa_status hswa_allocator_extend(hswa_allocator *alloc, int32_t seq, int64_t new_len);
+
+/* End of a prefill chunk (decode_step = 0) or of a decode step (decode_step =
+ * 1), after the kernels of that step: releases the SWA pages that lie wholly
+ * before the window of the next query (position len), i.e. logical pages
+ * below (len - W + 1) / PG; for decode steps only on every N-th call.
+ * *released (optional) receives the number of pages freed. */
+hswa_status hswa_allocator_step_end(hswa_allocator *alloc, int32_t seq, int32_t decode_step, int32_t *released);
+
+/* Request end: every page of `seq` goes back to its pool; the slot is free. */
+hswa_status hswa_allocator_free(hswa_allocator *alloc, int32_t seq);
+
+/* Block tables, host int32 [max_seqs][table_stride] each (either may be NULL):
+ * logical page -> FULL page / SWA page, -1 where nothing is held. */
+hswa_status hswa_allocator_tables(const hswa_allocator *alloc, int32_t *full_table, int32_t *swa_table);
+
+/* Pages held by sequence `seq` (seq >= 0) or by all sequences (seq < 0), and
+ * the free pages of each pool; any output may be NULL. */
+hswa_status hswa_allocator_usage(const hswa_allocator *alloc, int32_t seq, int64_t *full_used, int64_t *swa_used,
+                                 int64_t *full_free, int64_t *swa_free);
 
 #ifdef __cplusplus
 }

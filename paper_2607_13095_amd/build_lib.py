@@ -2,8 +2,9 @@
 
     python -m paper_2607_13095_amd.build_lib
 
-Each ``csrc/*.hip`` file is compiled with hipcc to an object under
-``_build/`` and the objects are linked into ``libhswa.so`` next to this file.
+Each ``csrc/*.hip`` file is compiled with hipcc (and each host-only
+``csrc/*.cpp`` file with the host C++ compiler) to an object under ``_build/``;
+the objects are linked into ``libhswa.so`` next to this file.
 """
 
 from __future__ import annotations
@@ -20,6 +21,9 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libhswa.so")
 SOURCES = ["api.hip", "kv_append.hip", "decode.hip", "prefill.hip"]
+HOST_SOURCES = ["allocator.cpp"]
+CXX = os.environ.get("CXX", shutil.which("g++") or "g++")
+CXXFLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-I", os.path.join(ROOT, "include")]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
@@ -46,6 +50,9 @@ def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     objs = [os.path.join(BUILD, s.replace(".hip", ".o")) for s in SOURCES]
     cmds = [[HIPCC, *FLAGS, "-c", os.path.join(CSRC, s), "-o", o] for s, o in zip(SOURCES, objs)]
+    host_objs = [os.path.join(BUILD, s.replace(".cpp", ".host.o")) for s in HOST_SOURCES]
+    cmds += [[CXX, *CXXFLAGS, "-c", os.path.join(CSRC, s), "-o", o] for s, o in zip(HOST_SOURCES, host_objs)]
+    objs += host_objs
     with cf.ThreadPoolExecutor(max_workers=min(len(cmds), 8)) as ex:
         for err in ex.map(_run, cmds):
             if verbose and err.strip():

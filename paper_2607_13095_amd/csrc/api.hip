@@ -48,7 +48,8 @@ hswa_status check_shape(const hswa_shape *sh) {
 
 hswa_status check_layer(hswa_layer layer) {
   if (layer.kind == HSWA_LAYER_FULL) return HSWA_OK;
-  if (layer.kind == HSWA_LAYER_SWA) return layer.window >= 1 ? HSWA_OK : HSWA_ERR_INVALID_ARG;
+  if (layer.kind == HSWA_LAYER_SWA || layer.kind == HSWA_LAYER_SWA_PAGED)
+    return layer.window >= 1 ? HSWA_OK : HSWA_ERR_INVALID_ARG;
   return HSWA_ERR_INVALID_ARG;
 }
 
@@ -67,6 +68,9 @@ hswa_status make_pool(hswa_layer layer, const hswa_shape *sh, const hswa_cache *
     pv.ring = hswa_ring_pages(layer.window, sh->page_size);
     pv.window = layer.window;
     if (pv.ring > cache->table_stride) return HSWA_ERR_CAPACITY;
+  } else if (layer.kind == HSWA_LAYER_SWA_PAGED) {  // FULL-style table, window masking
+    pv.ring = 0;
+    pv.window = layer.window;
   } else {
     pv.ring = 0;
     pv.window = 0;
@@ -204,7 +208,8 @@ hswa_status hswa_decode(hswa_layer layer, const hswa_shape *shape, const hswa_ca
   if (ns < 0 || max_context_len < 1) return HSWA_ERR_INVALID_ARG;
   hswa::PoolView pv{};
   if ((st = make_pool(layer, shape, cache, pv)) != HSWA_OK) return st;
-  if (layer.kind == HSWA_LAYER_FULL &&
+  // FULL-style tables are indexed by the logical page of every position
+  if ((layer.kind == HSWA_LAYER_FULL || layer.kind == HSWA_LAYER_SWA_PAGED) &&
       (int64_t)cache->table_stride * shape->page_size < (int64_t)max_context_len)
     return HSWA_ERR_CAPACITY;
   if (ns == 0) return HSWA_OK;

@@ -20,12 +20,15 @@ LIB_PATH = os.path.join(_PKG, "libhswa.so")
 
 HSWA_LAYER_FULL = 0
 HSWA_LAYER_SWA = 1
+HSWA_LAYER_SWA_PAGED = 2
 
 STATUS = {0: "HSWA_OK", -1: "HSWA_ERR_INVALID_ARG", -2: "HSWA_ERR_UNSUPPORTED", -3: "HSWA_ERR_CAPACITY",
           -4: "HSWA_ERR_LAUNCH"}
 
 EXPORTS = ["hswa_ring_pages", "hswa_page_bytes", "hswa_build_block_table", "hswa_kv_append", "hswa_prefill",
-           "hswa_decode_workspace_bytes", "hswa_decode_split_len", "hswa_decode", "hswa_status_string"]
+           "hswa_decode_workspace_bytes", "hswa_decode_split_len", "hswa_decode", "hswa_status_string",
+           "hswa_allocator_create", "hswa_allocator_destroy", "hswa_allocator_admit", "hswa_allocator_extend",
+           "hswa_allocator_step_end", "hswa_allocator_free", "hswa_allocator_tables", "hswa_allocator_usage"]
 
 
 class HswaError(RuntimeError):
@@ -41,6 +44,12 @@ class _Layer(ctypes.Structure):
 class _Shape(ctypes.Structure):
     _fields_ = [("num_q_heads", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("page_size", ctypes.c_int32), ("scale", ctypes.c_float)]
+
+
+class _AllocConfig(ctypes.Structure):
+    _fields_ = [("page_size", ctypes.c_int32), ("window", ctypes.c_int32), ("full_pages", ctypes.c_int64),
+                ("swa_pages", ctypes.c_int64), ("max_seqs", ctypes.c_int32), ("table_stride", ctypes.c_int32),
+                ("release_every", ctypes.c_int32)]
 
 
 class _Cache(ctypes.Structure):
@@ -76,6 +85,14 @@ def load():
         "hswa_decode_split_len": (I32, [SP, I32, I32]),
         "hswa_decode": (ctypes.c_int, [LP, SP, CP, P, P, I32, I32, P, SZ, P, P]),
         "hswa_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+        "hswa_allocator_create": (ctypes.c_int, [ctypes.POINTER(_AllocConfig), ctypes.POINTER(P)]),
+        "hswa_allocator_destroy": (None, [P]),
+        "hswa_allocator_admit": (ctypes.c_int, [P, I32, I64, I32]),
+        "hswa_allocator_extend": (ctypes.c_int, [P, I32, I64]),
+        "hswa_allocator_step_end": (ctypes.c_int, [P, I32, I32, P]),
+        "hswa_allocator_free": (ctypes.c_int, [P, I32]),
+        "hswa_allocator_tables": (ctypes.c_int, [P, P, P]),
+        "hswa_allocator_usage": (ctypes.c_int, [P, I32, P, P, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -89,10 +106,13 @@ def load():
 # ---------------------------------------------------------------------------
 
 class Layer:
-    """Layer-kind flag {SWA(W), FULL}."""
+    """Layer-kind flag {SWA(W), FULL}; "swa_paged" is an SWA layer over an
+    explicit-release (FULL-indexed) SWA block table from ``Allocator``."""
+
+    _KINDS = {"full": HSWA_LAYER_FULL, "swa": HSWA_LAYER_SWA, "swa_paged": HSWA_LAYER_SWA_PAGED}
 
     def __init__(self, kind: str, window: int = 0):
-        if kind not in ("full", "swa"):
+        if kind not in self._KINDS:
             raise ValueError(kind)
         self.kind, self.window = kind, int(window)
 
@@ -104,8 +124,12 @@ class Layer:
     def swa(cls, window: int):
         return cls("swa", window)
 
+    @classmethod
+    def swa_paged(cls, window: int):
+        return cls("swa_paged", window)
+
     def c(self):
-        return _Layer(HSWA_LAYER_SWA if self.kind == "swa" else HSWA_LAYER_FULL, self.window)
+        return _Layer(self._KINDS[self.kind], self.window)
 
 
 class Shape:
@@ -286,3 +310,61 @@ def decode(layer: Layer, shape: Shape, cache: Cache, q, context_lens, max_contex
     st = load().hswa_decode(layer.c(), ctypes.byref(sh), ctypes.byref(ca), qp, cp, ns, int(max_context_len), wp,
                             wbytes, o, _stream(stream))
     _check(st, "hswa_decode")
+
+
+# ---------------------------------------------------------------------------
+# explicit-release dual-pool allocator (host object)
+# ---------------------------------------------------------------------------
+
+class Allocator:
+    """Host page allocator of one FULL pool and one SWA pool (see
+    hswa_allocator_* in include/hswa.h); tables come back as numpy int32."""
+
+    def __init__(self, page_size, window, full_pages, swa_pages, max_seqs, table_stride, release_every=1):
+        self._lib = load()
+        self.cfg = _AllocConfig(int(page_size), int(window), int(full_pages), int(swa_pages), int(max_seqs),
+                                int(table_stride), int(release_every))
+        h = ctypes.c_void_p()
+        _check(self._lib.hswa_allocator_create(ctypes.byref(self.cfg), ctypes.byref(h)), "hswa_allocator_create")
+        self._h = h
+
+    def close(self):
+        if self._h:
+            self._lib.hswa_allocator_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def admit(self, seq, length, chunk):
+        """Returns the status (0 = admitted, HSWA_ERR_CAPACITY = -3 = a pool is short)."""
+        return int(self._lib.hswa_allocator_admit(self._h, int(seq), int(length), int(chunk)))
+
+    def extend(self, seq, new_len):
+        return int(self._lib.hswa_allocator_extend(self._h, int(seq), int(new_len)))
+
+    def step_end(self, seq, decode_step):
+        n = ctypes.c_int32(0)
+        _check(self._lib.hswa_allocator_step_end(self._h, int(seq), int(bool(decode_step)), ctypes.byref(n)),
+               "hswa_allocator_step_end")
+        return int(n.value)
+
+    def free(self, seq):
+        _check(self._lib.hswa_allocator_free(self._h, int(seq)), "hswa_allocator_free")
+
+    def tables(self):
+        ns, st = self.cfg.max_seqs, self.cfg.table_stride
+        full = np.empty((ns, st), dtype=np.int32)
+        swa = np.empty((ns, st), dtype=np.int32)
+        _check(self._lib.hswa_allocator_tables(self._h, full.ctypes.data, swa.ctypes.data), "hswa_allocator_tables")
+        return full, swa
+
+    def usage(self, seq=-1):
+        """(full_used, swa_used, full_free, swa_free) for one sequence or all."""
+        v = [ctypes.c_int64(0) for _ in range(4)]
+        _check(self._lib.hswa_allocator_usage(self._h, int(seq), *[ctypes.byref(x) for x in v]),
+               "hswa_allocator_usage")
+        return tuple(int(x.value) for x in v)
