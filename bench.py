@@ -387,6 +387,61 @@ def allocator_report(wl, reps=20):
             "full_pages_held": int(full_used), "host_us_per_decode_step": round(host_us, 1)}
 
 
+def prefix_tree_report(window=128, convs=128, turns=8, turn_len=512, seed=11):
+    """Window-safe prefix matching on a synthetic multi-turn workload: every
+    conversation grows turn by turn; after each turn the SWA slots before the
+    window of the next query are released (FULL slots stay). Continuing
+    requests match their whole history; requests that branch from an earlier
+    turn find FULL KV but no intact window there and are clipped. Reports host
+    cost per insert / match and the matched lengths."""
+    import time
+
+    from paper_2607_13095_amd import hswa
+
+    rng = np.random.default_rng(seed)
+    tree = hswa.PrefixTree(window)
+    hist = [[] for _ in range(convs)]
+    t_ins = t_match = t_rel = 0.0
+    n_ins = n_match = 0
+    cont_full = cont_safe = br_full = br_safe = 0
+    slot = 0
+    for t in range(turns):
+        for c in range(convs):
+            toks = hist[c] + [int(x) for x in rng.integers(0, 32000, turn_len)]
+            t0 = time.perf_counter()
+            fl, sl, _, _ = tree.match(toks)
+            t_match += time.perf_counter() - t0
+            n_match += 1
+            cont_full += fl
+            cont_safe += sl
+            n = len(toks)
+            slots = np.arange(slot, slot + n, dtype=np.int64)
+            slot += n
+            t0 = time.perf_counter()
+            tree.insert(toks, slots, slots)
+            t_ins += time.perf_counter() - t0
+            n_ins += 1
+            t0 = time.perf_counter()
+            tree.release_swa(toks, n - window + 1)
+            t_rel += time.perf_counter() - t0
+            hist[c] = toks
+    # branch requests: regenerate from the middle of an earlier turn
+    for c in range(convs):
+        cut = int(rng.integers(1, turns)) * turn_len - 7
+        fl, sl, _, _ = tree.match(hist[c][:cut] + [1, 2, 3])
+        br_full += fl
+        br_safe += sl
+    nodes, toks, swa_valid = tree.stats()
+    tree.close()
+    return {"window": window, "conversations": convs, "turns": turns, "turn_tokens": turn_len,
+            "cached_tokens": toks, "tokens_with_swa_slot": swa_valid, "nodes": nodes,
+            "continuing_hit_full": cont_full, "continuing_hit_window_safe": cont_safe,
+            "branch_hit_full": br_full, "branch_hit_window_safe": br_safe,
+            "host_us_per_match": round(t_match / n_match * 1e6, 1),
+            "host_us_per_insert": round(t_ins / n_ins * 1e6, 1),
+            "host_us_per_release": round(t_rel / n_ins * 1e6, 1)}
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -452,6 +507,10 @@ def main():
         del pb
         torch.cuda.empty_cache()
 
+    log("[bench] window-safe prefix tree")
+    prefix_rep = prefix_tree_report()
+    log(f"[bench] prefix tree: {prefix_rep}")
+
     log("[bench] explicit-release allocator")
     alloc_rep = allocator_report(wl)
     log(f"[bench] allocator: {alloc_rep}")
@@ -485,6 +544,7 @@ def main():
                      "kernel": "FULL-layer decode call: decode_kernel<true,true> + decode_merge_kernel"},
         "prefill": prefill,
         "allocator": alloc_rep,
+        "prefix_tree": prefix_rep,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

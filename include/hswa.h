@@ -274,6 +274,50 @@ hswa_status hswa_allocator_tables(const hswa_allocator *alloc, int32_t *full_tab
 hswa_status hswa_allocator_usage(const hswa_allocator *alloc, int32_t seq, int64_t *full_used, int64_t *swa_used,
                                  int64_t *full_free, int64_t *swa_free);
 
+/* ---- window-safe prefix cache tree (host) -------------------------------
+ * "SWA-Aware Prefix Cache Tree": a radix tree over token ids whose nodes carry
+ * per token two indices, the FULL KV slot and the SWA KV slot (-1 = none).
+ * Token equality is no longer enough for reuse: a match is the longest cached
+ * prefix whose tokens are equal and whose FULL slots are all held (full_len),
+ * clipped to the window-safe length (safe_len <= full_len): the largest P such
+ * that the W - 1 tokens before P, the cached keys the first new query at
+ * position P reads, all hold SWA slots. safe_len is the prefix length P to pass
+ * to hswa_prefill. SWA slots can be released on their own (out-of-window
+ * release) while FULL slots stay, or whole segments can be evicted.
+ * A tree is a host object owned by the caller; calls on one tree must not
+ * overlap. Slots are opaque to the tree (e.g. pool slots page * PG + offset). */
+typedef struct hswa_prefix_tree hswa_prefix_tree;
+
+hswa_status hswa_prefix_tree_create(int32_t window, hswa_prefix_tree **out);
+void hswa_prefix_tree_destroy(hswa_prefix_tree *tree);
+
+/* Caches tokens[0..n) with their slots (host arrays of n entries); positions
+ * already cached on this path take the new slots. */
+hswa_status hswa_prefix_tree_insert(hswa_prefix_tree *tree, const int32_t *tokens, int64_t n,
+                                    const int64_t *full_slots, const int64_t *swa_slots);
+
+/* Match of tokens[0..n): *full_len and *safe_len as above; if the slot outputs
+ * are non-NULL (n entries each) their first *full_len entries receive the
+ * matched slots. */
+hswa_status hswa_prefix_tree_match(const hswa_prefix_tree *tree, const int32_t *tokens, int64_t n,
+                                   int64_t *full_len, int64_t *safe_len, int64_t *full_slots_out,
+                                   int64_t *swa_slots_out);
+
+/* Out-of-window release: drops the SWA slots of positions [0, upto) of the
+ * cached path tokens[0..n) (FULL slots stay). *released = slots dropped. */
+hswa_status hswa_prefix_tree_release_swa(hswa_prefix_tree *tree, const int32_t *tokens, int64_t n, int64_t upto,
+                                         int64_t *released);
+
+/* Segment eviction: removes position `keep` of the cached path tokens[0..n)
+ * and everything cached after it (all continuations). *evicted = tokens
+ * removed. */
+hswa_status hswa_prefix_tree_evict(hswa_prefix_tree *tree, const int32_t *tokens, int64_t n, int64_t keep,
+                                   int64_t *evicted);
+
+/* Nodes, cached tokens and tokens with a valid SWA slot; outputs may be NULL. */
+hswa_status hswa_prefix_tree_stats(const hswa_prefix_tree *tree, int64_t *nodes, int64_t *tokens,
+                                   int64_t *swa_valid_tokens);
+
 #ifdef __cplusplus
 }
 #endif

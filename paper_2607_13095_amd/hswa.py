@@ -28,7 +28,10 @@ STATUS = {0: "HSWA_OK", -1: "HSWA_ERR_INVALID_ARG", -2: "HSWA_ERR_UNSUPPORTED", 
 EXPORTS = ["hswa_ring_pages", "hswa_page_bytes", "hswa_build_block_table", "hswa_kv_append", "hswa_prefill",
            "hswa_decode_workspace_bytes", "hswa_decode_split_len", "hswa_decode", "hswa_status_string",
            "hswa_allocator_create", "hswa_allocator_destroy", "hswa_allocator_admit", "hswa_allocator_extend",
-           "hswa_allocator_step_end", "hswa_allocator_free", "hswa_allocator_tables", "hswa_allocator_usage"]
+           "hswa_allocator_step_end", "hswa_allocator_free", "hswa_allocator_tables", "hswa_allocator_usage",
+           "hswa_prefix_tree_create", "hswa_prefix_tree_destroy", "hswa_prefix_tree_insert",
+           "hswa_prefix_tree_match", "hswa_prefix_tree_release_swa", "hswa_prefix_tree_evict",
+           "hswa_prefix_tree_stats"]
 
 
 class HswaError(RuntimeError):
@@ -93,6 +96,13 @@ def load():
         "hswa_allocator_free": (ctypes.c_int, [P, I32]),
         "hswa_allocator_tables": (ctypes.c_int, [P, P, P]),
         "hswa_allocator_usage": (ctypes.c_int, [P, I32, P, P, P, P]),
+        "hswa_prefix_tree_create": (ctypes.c_int, [I32, ctypes.POINTER(P)]),
+        "hswa_prefix_tree_destroy": (None, [P]),
+        "hswa_prefix_tree_insert": (ctypes.c_int, [P, P, I64, P, P]),
+        "hswa_prefix_tree_match": (ctypes.c_int, [P, P, I64, P, P, P, P]),
+        "hswa_prefix_tree_release_swa": (ctypes.c_int, [P, P, I64, I64, P]),
+        "hswa_prefix_tree_evict": (ctypes.c_int, [P, P, I64, I64, P]),
+        "hswa_prefix_tree_stats": (ctypes.c_int, [P, P, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -367,4 +377,75 @@ class Allocator:
         v = [ctypes.c_int64(0) for _ in range(4)]
         _check(self._lib.hswa_allocator_usage(self._h, int(seq), *[ctypes.byref(x) for x in v]),
                "hswa_allocator_usage")
+        return tuple(int(x.value) for x in v)
+
+
+# ---------------------------------------------------------------------------
+# window-safe prefix cache tree (host object)
+# ---------------------------------------------------------------------------
+
+def _i32_arr(x):
+    return np.ascontiguousarray(np.asarray(x, dtype=np.int32))
+
+
+def _i64_arr(x):
+    return np.ascontiguousarray(np.asarray(x, dtype=np.int64))
+
+
+class PrefixTree:
+    """Radix tree with per-token FULL and SWA slots (hswa_prefix_tree_*)."""
+
+    def __init__(self, window):
+        self._lib = load()
+        h = ctypes.c_void_p()
+        _check(self._lib.hswa_prefix_tree_create(int(window), ctypes.byref(h)), "hswa_prefix_tree_create")
+        self._h, self.window = h, int(window)
+
+    def close(self):
+        if self._h:
+            self._lib.hswa_prefix_tree_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def insert(self, tokens, full_slots, swa_slots):
+        t, f, s = _i32_arr(tokens), _i64_arr(full_slots), _i64_arr(swa_slots)
+        if not (t.size == f.size == s.size):
+            raise ValueError("one slot per token")
+        _check(self._lib.hswa_prefix_tree_insert(self._h, t.ctypes.data, t.size, f.ctypes.data, s.ctypes.data),
+               "hswa_prefix_tree_insert")
+
+    def match(self, tokens):
+        """(full_len, safe_len, full_slots[:full_len], swa_slots[:full_len])."""
+        t = _i32_arr(tokens)
+        fo = np.full(max(1, t.size), -2, dtype=np.int64)
+        so = np.full(max(1, t.size), -2, dtype=np.int64)
+        fl, sl = ctypes.c_int64(0), ctypes.c_int64(0)
+        _check(self._lib.hswa_prefix_tree_match(self._h, t.ctypes.data, t.size, ctypes.byref(fl), ctypes.byref(sl),
+                                                fo.ctypes.data, so.ctypes.data), "hswa_prefix_tree_match")
+        n = int(fl.value)
+        return n, int(sl.value), fo[:n].copy(), so[:n].copy()
+
+    def release_swa(self, tokens, upto):
+        t = _i32_arr(tokens)
+        r = ctypes.c_int64(0)
+        _check(self._lib.hswa_prefix_tree_release_swa(self._h, t.ctypes.data, t.size, int(upto), ctypes.byref(r)),
+               "hswa_prefix_tree_release_swa")
+        return int(r.value)
+
+    def evict(self, tokens, keep):
+        t = _i32_arr(tokens)
+        r = ctypes.c_int64(0)
+        _check(self._lib.hswa_prefix_tree_evict(self._h, t.ctypes.data, t.size, int(keep), ctypes.byref(r)),
+               "hswa_prefix_tree_evict")
+        return int(r.value)
+
+    def stats(self):
+        """(nodes, cached tokens, tokens with a valid SWA slot)."""
+        v = [ctypes.c_int64(0) for _ in range(3)]
+        _check(self._lib.hswa_prefix_tree_stats(self._h, *[ctypes.byref(x) for x in v]), "hswa_prefix_tree_stats")
         return tuple(int(x.value) for x in v)
