@@ -387,6 +387,64 @@ def allocator_report(wl, reps=20):
             "full_pages_held": int(full_used), "host_us_per_decode_step": round(host_us, 1)}
 
 
+def prefetch_report(pb, layers=70, depth=2, reps=3):
+    """Layerwise host-to-device prefetch on the chunked-prefill workload: a
+    70-layer stack (FULL iff layer % 7 == 6) whose layer pools are loaded from
+    pinned host memory into a ring of `depth` device slots per kind. Times the
+    stack with data resident (attention only), with copy-then-compute per
+    layer on one stream, and with the copies on a stream running ahead."""
+    import torch
+
+    from paper_2607_13095_amd import hswa
+    from paper_2607_13095_amd.prefetch import LayerPlan, LayerwisePrefetch
+
+    kinds = ["full" if l % 7 == 6 else "swa" for l in range(layers)]
+    by_kind = {L["kind"]: L for L in pb.layers}
+    host, rings = {}, {}
+    for k, L in by_kind.items():
+        kp, vp = L["kv"].k_pool, L["kv"].v_pool
+        host[k] = (torch.empty(kp.shape, dtype=kp.dtype, pin_memory=True),
+                   torch.empty(vp.shape, dtype=vp.dtype, pin_memory=True))
+        host[k][0].copy_(kp)
+        host[k][1].copy_(vp)
+        rings[k] = [(torch.empty_like(kp), torch.empty_like(vp)) for _ in range(depth)]
+    plans = [LayerPlan(k, host[k]) for k in kinds]
+    h2d_bytes = sum(sum(t.numel() * t.element_size() for t in host[k]) for k in kinds)
+
+    def compute(l, slot):
+        L = by_kind[kinds[l]]
+        cache = hswa.Cache(slot[0], slot[1], L["kv"].block_table)
+        hswa.prefill(L["layer"], pb.shape, cache, L["q"], L["kn"], L["vn"], pb.cu, pb.pre, pb.maxc, L["out"])
+
+    def resident(l, _slot):
+        pb.call(by_kind[kinds[l]])
+
+    pf = LayerwisePrefetch(rings, depth)
+
+    def timed(fn):
+        fn()  # warm-up
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b))
+        return float(np.median(ts))
+
+    t_att = timed(lambda: [resident(l, None) for l in range(layers)])
+    t_serial = timed(lambda: pf.run(plans, compute, overlap=False))
+    t_over = timed(lambda: pf.run(plans, compute, overlap=True))
+    copy_ms = max(t_serial - t_att, 1e-6)
+    return {"layers": layers, "depth": depth, "h2d_bytes_per_stack": int(h2d_bytes),
+            "attention_only_ms": round(t_att, 3), "copy_then_compute_ms": round(t_serial, 3),
+            "layerwise_prefetch_ms": round(t_over, 3),
+            "h2d_gbs_serial": round(h2d_bytes / (copy_ms * 1e-3) / 1e9, 1),
+            "copy_hidden_frac": round((t_serial - t_over) / copy_ms, 3)}
+
+
 def prefix_tree_report(window=128, convs=128, turns=8, turn_len=512, seed=11):
     """Window-safe prefix matching on a synthetic multi-turn workload: every
     conversation grows turn by turn; after each turn the SWA slots before the
@@ -504,6 +562,9 @@ def main():
                          "algorithmic_flops": pb.flops["full"]},
         }
         log(f"[bench] prefill FULL {f_ms:.3f} ms = {f_tf:.1f} TFLOP/s; SWA {s_ms:.3f} ms = {s_gbs:.0f} GB/s")
+        log("[bench] layerwise prefetch (70-layer prefill stack, prefix from pinned host memory)")
+        prefill["prefetch"] = prefetch_report(pb)
+        log(f"[bench] prefetch: {prefill['prefetch']}")
         del pb
         torch.cuda.empty_cache()
 
