@@ -113,19 +113,19 @@ def copy_calibration():
 # ----------------------------------------------------------------------------
 
 class DecodeBench:
-    def __init__(self, wl):
+    def __init__(self, wl, nq=1):
         import torch
 
         import synth
         from paper_2607_13095_amd import hswa
         from paper_2607_13095_amd.kvcache import LayerKV, pages_for
 
-        self.wl = wl
+        self.wl, self.nq = wl, int(nq)
         dev = "cuda"
         hq, hkv, d, pg, W = wl.hq, wl.hkv, wl.head_dim, wl.page_size, wl.window
         ns = wl.ns
         self.ctx = np.asarray(wl.prefix, dtype=np.int64)          # cached tokens c_b
-        self.final = (self.ctx + 1).tolist()                       # context incl. the new token
+        self.final = (self.ctx + nq).tolist()                      # context incl. the nq new tokens
         self.shape = hswa.Shape(hq, hkv, d, pg)
         self.maxc = int(max(self.final))
         i32 = lambda x: torch.as_tensor(np.asarray(x, dtype=np.int32), device=dev)  # noqa: E731
@@ -140,29 +140,30 @@ class DecodeBench:
             v_hist = synth.torch_normal_bf16((T, hkv, d), dev, wl.seed, li, 0, synth.TAG_V)
             cu = synth.cu_seqlens(self.ctx)
             hswa.kv_append(layer, self.shape, kv.cache, k_hist, v_hist, i32(cu), i32(np.zeros(ns)))
-            k_new = synth.torch_normal_bf16((ns, hkv, d), dev, wl.seed, li, 0, synth.TAG_KDEC)
-            v_new = synth.torch_normal_bf16((ns, hkv, d), dev, wl.seed, li, 0, synth.TAG_VDEC)
-            q = synth.torch_normal_bf16((ns, hq, d), dev, wl.seed, li, 0, synth.TAG_QDEC)
-            out = torch.empty((ns, hq, d), dtype=torch.bfloat16, device=dev)
-            wsb = hswa.decode_workspace_bytes(self.shape, ns, self.maxc) if kind == "full" else 0
+            k_new = synth.torch_normal_bf16((ns * nq, hkv, d), dev, wl.seed, li, 0, synth.TAG_KDEC)
+            v_new = synth.torch_normal_bf16((ns * nq, hkv, d), dev, wl.seed, li, 0, synth.TAG_VDEC)
+            qshape = (ns, hq, d) if nq == 1 else (ns, nq, hq, d)
+            q = synth.torch_normal_bf16(qshape, dev, wl.seed, li, 0, synth.TAG_QDEC)
+            out = torch.empty(qshape, dtype=torch.bfloat16, device=dev)
+            wsb = hswa.decode_multi_workspace_bytes(self.shape, ns, nq, self.maxc) if kind == "full" else 0
             ws = torch.empty(max(1, wsb), dtype=torch.uint8, device=dev)
             self.layers.append(dict(kind=kind, layer=layer, kv=kv, k_hist=k_hist, v_hist=v_hist, cu=cu,
                                     k_new=k_new, v_new=v_new, q=q, out=out, ws=ws))
-        self.cu1 = i32(np.arange(ns + 1))
+        self.cu1 = i32(np.arange(ns + 1) * nq)
         self.start = i32(self.ctx)
         self.ctx_lens = i32(self.final)
         torch.cuda.synchronize()
         # algorithmic bytes
         row = hkv * d * 2 * 2                                      # K + V bytes per key
-        qo = 2 * ns * hq * d * 2
+        qo = 2 * ns * nq * hq * d * 2
         self.bytes = {}
         for L in self.layers:
             if L["kind"] == "full":
-                keys = int(np.sum(self.ctx + 1))
+                keys = int(np.sum(self.ctx + nq))
             else:
-                keys = int(np.sum(np.minimum(W, self.ctx + 1)))
+                keys = int(np.sum(np.minimum(W + nq - 1, self.ctx + nq)))
             self.bytes[L["kind"]] = keys * row + qo
-        self.append_bytes = len(self.layers) * ns * hkv * d * 2 * 2 * 2   # read + write
+        self.append_bytes = len(self.layers) * ns * nq * hkv * d * 2 * 2 * 2   # read + write
 
     def step(self, full_events=None):
         from paper_2607_13095_amd import hswa
@@ -171,24 +172,26 @@ class DecodeBench:
             hswa.kv_append(L["layer"], self.shape, L["kv"].cache, L["k_new"], L["v_new"], self.cu1, self.start)
             if L["kind"] == "full" and full_events is not None:
                 full_events[0].record()
-            hswa.decode(L["layer"], self.shape, L["kv"].cache, L["q"], self.ctx_lens, self.maxc, L["out"],
-                        workspace=L["ws"])
+            self.decode(L)
             if L["kind"] == "full" and full_events is not None:
                 full_events[1].record()
+
+    def decode(self, L):
+        from paper_2607_13095_amd import hswa
+
+        fn = hswa.decode if self.nq == 1 else hswa.decode_multi
+        fn(L["layer"], self.shape, L["kv"].cache, L["q"], self.ctx_lens, self.maxc, L["out"], workspace=L["ws"])
 
     def time_kind(self, kind, reps=20):
         """Event timing of one layer kind's decode call alone (median of reps)."""
         import torch
-
-        from paper_2607_13095_amd import hswa
 
         L = next(x for x in self.layers if x["kind"] == kind)
         ts = []
         for _ in range(reps):
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record()
-            hswa.decode(L["layer"], self.shape, L["kv"].cache, L["q"], self.ctx_lens, self.maxc, L["out"],
-                        workspace=L["ws"])
+            self.decode(L)
             b.record()
             b.synchronize()
             ts.append(a.elapsed_time(b))
@@ -568,6 +571,20 @@ def main():
         del pb
         torch.cuda.empty_cache()
 
+    log("[bench] multi-query decode (1 + 3 queries per sequence)")
+    mt = DecodeBench(wl, nq=4)
+    for _ in range(3):
+        mt.step()
+    torch.cuda.synchronize()
+    mt_full = mt.time_kind("full")
+    mt_swa = mt.time_kind("swa")
+    mtp = {"queries_per_seq": 4, "full_ms": round(mt_full, 5), "swa_ms": round(mt_swa, 5),
+           "full_gbs": round(mt.bytes["full"] / (mt_full * 1e-3) / 1e9, 1),
+           "full_ms_vs_one_query": round(mt_full / full_avg, 3)}
+    log(f"[bench] multi-query decode: {mtp}")
+    del mt
+    torch.cuda.empty_cache()
+
     log("[bench] window-safe prefix tree")
     prefix_rep = prefix_tree_report()
     log(f"[bench] prefix tree: {prefix_rep}")
@@ -604,6 +621,7 @@ def main():
                      "algorithmic_bytes": db.bytes["full"],
                      "kernel": "FULL-layer decode call: decode_kernel<true,true> + decode_merge_kernel"},
         "prefill": prefill,
+        "multi_query_decode": mtp,
         "allocator": alloc_rep,
         "prefix_tree": prefix_rep,
         "cpu_baseline": cpu,

@@ -208,6 +208,23 @@ hswa_status hswa_decode(hswa_layer layer, const hswa_shape *shape, const hswa_ca
                         void *out, void *stream);
 
 /* Static string naming a status. */
+/* Multi-query decode ("MTP Optimization": the model verifies 1 + 3 predicted
+ * tokens per sequence per step): num_queries (1 .. 64) new queries per
+ * sequence at positions c_b - num_queries .. c_b - 1, where c_b =
+ * context_lens[b] counts the cached tokens including all new ones (append them
+ * first). Query i attends keys lo .. its own position (causal among the new
+ * tokens; lo as in hswa_decode for its own position). Queries whose position
+ * is negative get zero rows.
+ * q, out: device bf16 [ns][num_queries][Hq][D]; workspace >=
+ * hswa_decode_multi_workspace_bytes (FULL only). num_queries = 1 is exactly
+ * hswa_decode. */
+size_t hswa_decode_multi_workspace_bytes(const hswa_shape *shape, int32_t ns, int32_t num_queries,
+                                         int32_t max_context_len);
+hswa_status hswa_decode_multi(hswa_layer layer, const hswa_shape *shape, const hswa_cache *cache,
+                              const void *q, const int32_t *context_lens, int32_t ns, int32_t num_queries,
+                              int32_t max_context_len, void *workspace, size_t workspace_bytes, void *out,
+                              void *stream);
+
 const char *hswa_status_string(hswa_status status);
 
 /* ---- explicit-release dual-pool page allocator (host) -------------------

@@ -87,14 +87,16 @@ struct DecodeGeometry {
   size_t total_bytes;
 };
 
-DecodeGeometry decode_geometry(const hswa_shape *sh, int32_t ns, int32_t max_ctx) {
+constexpr int32_t kMaxQueries = 64;  // queries per sequence in one decode call
+
+DecodeGeometry decode_geometry(const hswa_shape *sh, int32_t ns, int32_t max_ctx, int32_t nq) {
   DecodeGeometry g{};
   const int group = sh->num_q_heads / sh->num_kv_heads;
   g.split_len = hswa::decode_split_len(ns, sh->num_kv_heads, group, max_ctx);
   g.max_splits = (max_ctx + g.split_len - 1) / g.split_len;
   if (g.max_splits < 1) g.max_splits = 1;
   if (g.max_splits == 1) return g;  // single pass, no workspace
-  const size_t rows = (size_t)ns * sh->num_q_heads * g.max_splits;
+  const size_t rows = (size_t)ns * nq * sh->num_q_heads * g.max_splits;
   g.o_bytes = align_up(rows * sh->head_dim * sizeof(float), 256);
   g.total_bytes = g.o_bytes + align_up(rows * sizeof(float), 256);
   return g;
@@ -188,24 +190,30 @@ hswa_status hswa_prefill(hswa_layer layer, const hswa_shape *shape, const hswa_c
   return finish_launch(hswa::launch_prefill(p, s), s);
 }
 
-size_t hswa_decode_workspace_bytes(const hswa_shape *shape, int32_t ns, int32_t max_context_len) {
+size_t hswa_decode_multi_workspace_bytes(const hswa_shape *shape, int32_t ns, int32_t num_queries,
+                                         int32_t max_context_len) {
   if (check_shape(shape) != HSWA_OK || ns < 0 || max_context_len < 1) return 0;
+  if (num_queries < 1 || num_queries > kMaxQueries) return 0;
   if (ns == 0) return 0;
-  return decode_geometry(shape, ns, max_context_len).total_bytes;
+  return decode_geometry(shape, ns, max_context_len, num_queries).total_bytes;
+}
+
+size_t hswa_decode_workspace_bytes(const hswa_shape *shape, int32_t ns, int32_t max_context_len) {
+  return hswa_decode_multi_workspace_bytes(shape, ns, 1, max_context_len);
 }
 
 int32_t hswa_decode_split_len(const hswa_shape *shape, int32_t ns, int32_t max_context_len) {
   if (check_shape(shape) != HSWA_OK || ns < 1 || max_context_len < 1) return -1;
-  return decode_geometry(shape, ns, max_context_len).split_len;
+  return decode_geometry(shape, ns, max_context_len, 1).split_len;
 }
 
-hswa_status hswa_decode(hswa_layer layer, const hswa_shape *shape, const hswa_cache *cache, const void *q,
-                        const int32_t *context_lens, int32_t ns, int32_t max_context_len, void *workspace,
-                        size_t workspace_bytes, void *out, void *stream) {
+hswa_status hswa_decode_multi(hswa_layer layer, const hswa_shape *shape, const hswa_cache *cache, const void *q,
+                              const int32_t *context_lens, int32_t ns, int32_t num_queries, int32_t max_context_len,
+                              void *workspace, size_t workspace_bytes, void *out, void *stream) {
   hswa_status st;
   if ((st = check_layer(layer)) != HSWA_OK) return st;
   if ((st = check_shape(shape)) != HSWA_OK) return st;
-  if (ns < 0 || max_context_len < 1) return HSWA_ERR_INVALID_ARG;
+  if (ns < 0 || max_context_len < 1 || num_queries < 1 || num_queries > kMaxQueries) return HSWA_ERR_INVALID_ARG;
   hswa::PoolView pv{};
   if ((st = make_pool(layer, shape, cache, pv)) != HSWA_OK) return st;
   // FULL-style tables are indexed by the logical page of every position
@@ -224,9 +232,10 @@ hswa_status hswa_decode(hswa_layer layer, const hswa_shape *shape, const hswa_ca
   p.hkv = shape->num_kv_heads;
   p.group = p.hq / p.hkv;
   p.max_ctx = max_context_len;
+  p.nq = num_queries;
   p.scale_log2 = shape->scale * 1.4426950408889634f;
   if (layer.kind == HSWA_LAYER_FULL) {
-    const DecodeGeometry geo = decode_geometry(shape, ns, max_context_len);
+    const DecodeGeometry geo = decode_geometry(shape, ns, max_context_len, num_queries);
     p.split_len = geo.split_len;
     p.max_splits = geo.max_splits;
     if (geo.max_splits > 1) {
@@ -241,6 +250,13 @@ hswa_status hswa_decode(hswa_layer layer, const hswa_shape *shape, const hswa_ca
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
   return finish_launch(hswa::launch_decode(p, s), s);
+}
+
+hswa_status hswa_decode(hswa_layer layer, const hswa_shape *shape, const hswa_cache *cache, const void *q,
+                        const int32_t *context_lens, int32_t ns, int32_t max_context_len, void *workspace,
+                        size_t workspace_bytes, void *out, void *stream) {
+  return hswa_decode_multi(layer, shape, cache, q, context_lens, ns, 1, max_context_len, workspace, workspace_bytes,
+                           out, stream);
 }
 
 const char *hswa_status_string(hswa_status status) {

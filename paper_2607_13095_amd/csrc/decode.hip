@@ -69,7 +69,8 @@ __global__ __launch_bounds__(kWave) void decode_kernel(DecodeParams p) {
   const int shift = pv.pg_shift;
   const int pg = 1 << shift;
   const float c2 = p.scale_log2;
-  const int hchunks = (p.group + kCols - 1) / kCols;
+  const int ncols = p.nq * p.group;  // (query, head) pairs of one KV head
+  const int hchunks = (ncols + kCols - 1) / kCols;
 
   // Loop-invariant byte offsets of this lane's operands inside one page-head
   // (used when a 32-key chunk never straddles two pages, i.e. PG >= 32).
@@ -122,39 +123,46 @@ __global__ __launch_bounds__(kWave) void decode_kernel(DecodeParams p) {
   {
     const int g = gy / hchunks;
     const int hc = gy - g * hchunks;
-    const int nheads = min(kCols, p.group - hc * kCols);
-    const int head0 = g * p.group + hc * kCols;
-    const int64_t row = (int64_t)b * p.hq + head0 + r;  // this lane's output row (if r < nheads)
+    // this lane's MFMA column: query qi of the sequence, head hh of KV head g's group
+    const int col = hc * kCols + r;
+    const bool colv = col < ncols;
+    const int qi = colv ? col / p.group : 0;
+    const int hh = colv ? col - qi * p.group : 0;
+    const int64_t row = ((int64_t)b * p.nq + qi) * p.hq + (int64_t)g * p.group + hh;  // output row (if colv)
 
     const int ctx = min(p.ctx_lens[b], p.max_ctx);
     if (ctx < 1) {
-      if (!kSplit && r < nheads) {
+      if (!kSplit && colv) {
         const u32x2 z = {0u, 0u};
 #pragma unroll
         for (int dt = 0; dt < 8; ++dt) *reinterpret_cast<u32x2 *>(p.out + row * kHeadDim + 16 * dt + 4 * q) = z;
       }
       return;
     }
-    const int pos = ctx - 1;
-    int kb, ke;
+    const int pos = ctx - 1;       // the last query's position
+    const int pos0 = ctx - p.nq;   // the first query's position
+    int kb, ke;                    // the item's key range (union over its columns)
     if (kSplit) {
       kb = split * p.split_len;
       ke = min(pos, kb + p.split_len - 1);
     } else {
-      kb = pv.window > 0 ? max(0, pos - pv.window + 1) : 0;
+      kb = pv.window > 0 ? max(0, pos0 - pv.window + 1) : 0;
       ke = pos;
     }
+    // keys this lane's column may see: causal among the queries, and its own window
+    const int cpos = pos0 + qi;
+    const int ckb = max(kb, pv.window > 0 ? max(0, cpos - pv.window + 1) : 0);
+    const int cke = min(ke, cpos);
 
-    // Q^T operand: lane holds head r, dims 32t + 8q .. +7 for step t.
+    // Q^T operand: lane holds column r, dims 32t + 8q .. +7 for step t.
     u32x4 qf[4];
     {
-      const bool hv = r < nheads;
-      const uint16_t *qrow = p.q + ((int64_t)b * p.hq + head0 + (hv ? r : 0)) * kHeadDim;
+      const uint16_t *qrow = p.q + (colv ? row : (int64_t)b * p.nq * p.hq) * kHeadDim;
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         const u32x4 v = ldg128(qrow + 32 * t + 8 * q);
         const u32x4 z = {0u, 0u, 0u, 0u};
-        qf[t] = hv ? v : z;
+        qf[t] = colv ? v : z;
       }
     }
 
@@ -234,15 +242,22 @@ __global__ __launch_bounds__(kWave) void decode_kernel(DecodeParams p) {
         sa = mfma16x16x32(ch.ka[t], qf[t], sa);
         sb = mfma16x16x32(ch.kb[t], qf[t], sb);
       }
+      // keep: keys of the item range (V rows outside it are zeroed below);
+      // sk: those this lane's column sees
       keep = 0;
+      uint32_t sk = 0;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) keep |= (uint32_t)(ch.kv0 + i >= kb && ch.kv0 + i <= ke) << i;
+      for (int i = 0; i < 8; ++i) {
+        keep |= (uint32_t)(ch.kv0 + i >= kb && ch.kv0 + i <= ke) << i;
+        sk |= (uint32_t)(ch.kv0 + i >= ckb && ch.kv0 + i <= cke) << i;
+      }
       if (!ch.vok) keep = 0;
+      sk &= keep;
       float s[8];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        s[i] = (keep >> i) & 1u ? sa[i] : -INFINITY;
-        s[4 + i] = (keep >> (4 + i)) & 1u ? sb[i] : -INFINITY;
+        s[i] = (sk >> i) & 1u ? sa[i] : -INFINITY;
+        s[4 + i] = (sk >> (4 + i)) & 1u ? sb[i] : -INFINITY;
       }
       const float cmax = max_xor32(max_xor16(max8(s)));
       const float mnew = fmaxf(m, cmax);
@@ -307,8 +322,10 @@ __global__ __launch_bounds__(kWave) void decode_kernel(DecodeParams p) {
 
     // Normalise and write: lane holds O^T[d = 16 dt + 4 q + i][head r].
     lsum = sum_xor32(sum_xor16(lsum));
-    if (r < nheads) {
-      const float inv = 1.f / lsum;
+    if (colv) {
+      // a column that sees no key of this piece (a later query's last keys)
+      // writes o = 0 with log-sum-exp -inf: weight 0 in the merge
+      const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
       if (kSplit) {
         float *dst = p.ws_o + (row * p.max_splits + split) * kHeadDim + 4 * q;
 #pragma unroll
@@ -334,8 +351,8 @@ __global__ __launch_bounds__(kWave) void decode_kernel(DecodeParams p) {
 __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(DecodeParams p) {
   const int lane = threadIdx.x & (kWave - 1);
   const int64_t idx = (int64_t)blockIdx.x * (kMergeThreads / kWave) + (threadIdx.x / kWave);
-  if (idx >= (int64_t)p.ns * p.hq) return;
-  const int b = (int)(idx / p.hq);
+  if (idx >= (int64_t)p.ns * p.nq * p.hq) return;
+  const int b = (int)(idx / ((int64_t)p.nq * p.hq));
   const int ctx = min(p.ctx_lens[b], p.max_ctx);
   uint32_t *dst = reinterpret_cast<uint32_t *>(p.out + idx * kHeadDim) + lane;
   if (ctx < 1) {
@@ -394,20 +411,20 @@ int32_t decode_split_len(int32_t ns, int32_t hkv, int32_t group, int32_t max_ctx
 
 hipError_t launch_decode(const DecodeParams &p, hipStream_t stream) {
   if (p.ns <= 0) return hipSuccess;
-  const int hchunks = (p.group + kCols - 1) / kCols;
+  const int hchunks = (p.nq * p.group + kCols - 1) / kCols;
   const int64_t items = (int64_t)p.ns * p.hkv * hchunks * p.max_splits;  // upper bound
   const unsigned grid = (unsigned)items;
   // One-page path: 32-key chunks never straddle pages (PG >= 32) and every key
   // range fits the 64-entry lane table.
   const int64_t range = p.max_splits > 1 ? p.split_len
-                                         : (p.pool.window > 0 ? min(p.pool.window, p.max_ctx) : p.max_ctx);
+                                         : (p.pool.window > 0 ? min(p.pool.window + p.nq - 1, p.max_ctx) : p.max_ctx);
   const int64_t range_pages = ((range + (1 << p.pool.pg_shift) - 1) >> p.pool.pg_shift) + 1;
   const bool one_page = p.pool.pg_shift >= 5 && range_pages < kWave;
   if (p.max_splits > 1) {
     const hipError_t e = one_page ? launch_kernel(decode_kernel<true, true>, dim3(grid), dim3(kWave), stream, p)
                                   : launch_kernel(decode_kernel<true, false>, dim3(grid), dim3(kWave), stream, p);
     if (e != hipSuccess) return e;
-    const int64_t rows = (int64_t)p.ns * p.hq;
+    const int64_t rows = (int64_t)p.ns * p.nq * p.hq;
     const int per_block = kMergeThreads / kWave;
     return launch_kernel(decode_merge_kernel, dim3((unsigned)((rows + per_block - 1) / per_block)),
                          dim3(kMergeThreads), stream, p);

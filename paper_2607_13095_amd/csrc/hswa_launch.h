@@ -42,9 +42,10 @@ struct DecodeParams {
   const uint16_t *q;      // [ns][Hq][D]
   const int32_t *ctx_lens;
   uint16_t *out;          // [ns][Hq][D]
-  float *ws_o;            // FULL split partials [ns][Hq][max_splits][D]
-  float *ws_lse;          // [ns][Hq][max_splits]
+  float *ws_o;            // FULL split partials [ns * nq * Hq][max_splits][D]
+  float *ws_lse;          // [ns * nq * Hq][max_splits]
   int32_t ns, hq, hkv, group, max_ctx;
+  int32_t nq;             // queries per sequence, at positions ctx - nq .. ctx - 1 (q, out: [ns][nq][Hq][D])
   int32_t split_len, max_splits;  // max_splits == 1 => single pass, no workspace
   float scale_log2;       // scale * log2(e)
 };

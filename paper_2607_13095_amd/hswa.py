@@ -31,7 +31,7 @@ EXPORTS = ["hswa_ring_pages", "hswa_page_bytes", "hswa_build_block_table", "hswa
            "hswa_allocator_step_end", "hswa_allocator_free", "hswa_allocator_tables", "hswa_allocator_usage",
            "hswa_prefix_tree_create", "hswa_prefix_tree_destroy", "hswa_prefix_tree_insert",
            "hswa_prefix_tree_match", "hswa_prefix_tree_release_swa", "hswa_prefix_tree_evict",
-           "hswa_prefix_tree_stats"]
+           "hswa_prefix_tree_stats", "hswa_decode_multi_workspace_bytes", "hswa_decode_multi"]
 
 
 class HswaError(RuntimeError):
@@ -88,6 +88,8 @@ def load():
         "hswa_decode_split_len": (I32, [SP, I32, I32]),
         "hswa_decode": (ctypes.c_int, [LP, SP, CP, P, P, I32, I32, P, SZ, P, P]),
         "hswa_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+        "hswa_decode_multi_workspace_bytes": (SZ, [SP, I32, I32, I32]),
+        "hswa_decode_multi": (ctypes.c_int, [LP, SP, CP, P, P, I32, I32, I32, P, SZ, P, P]),
         "hswa_allocator_create": (ctypes.c_int, [ctypes.POINTER(_AllocConfig), ctypes.POINTER(P)]),
         "hswa_allocator_destroy": (None, [P]),
         "hswa_allocator_admit": (ctypes.c_int, [P, I32, I64, I32]),
@@ -300,6 +302,36 @@ def prefill(layer: Layer, shape: Shape, cache: Cache, q, k_new, v_new, cu_seqlen
     st = load().hswa_prefill(layer.c(), ctypes.byref(sh), ctypes.byref(ca), *args, ns, t, int(max_chunk_len), o,
                              _stream(stream))
     _check(st, "hswa_prefill")
+
+
+def decode_multi_workspace_bytes(shape: Shape, ns: int, num_queries: int, max_context_len: int) -> int:
+    sh = shape.c()
+    return int(load().hswa_decode_multi_workspace_bytes(ctypes.byref(sh), int(ns), int(num_queries),
+                                                        int(max_context_len)))
+
+
+def decode_multi(layer: Layer, shape: Shape, cache: Cache, q, context_lens, max_context_len: int, out,
+                 workspace=None, stream=None):
+    """Multi-query decode; q, out [NS, nq, Hq, D]; see hswa_decode_multi."""
+    import torch
+
+    if q.dim() != 4:
+        raise ValueError("q must be [NS, num_queries, Hq, D]")
+    ns, nq = int(q.shape[0]), int(q.shape[1])
+    if int(context_lens.numel()) != ns:
+        raise ValueError("one context length per sequence")
+    row = nq * shape.num_q_heads * shape.head_dim
+    qp = _ptr(q, "q", _bf16(), ns * row)
+    cp = _ptr(context_lens, "context_lens", _i32(), ns)
+    o = _ptr(out, "out", _bf16(), ns * row)
+    wp, wbytes = None, 0
+    if workspace is not None:
+        wp = _ptr(workspace, "workspace", (torch.uint8, torch.float32, torch.int32))
+        wbytes = workspace.numel() * workspace.element_size()
+    sh, ca = shape.c(), cache.c()
+    st = load().hswa_decode_multi(layer.c(), ctypes.byref(sh), ctypes.byref(ca), qp, cp, ns, nq,
+                                  int(max_context_len), wp, wbytes, o, _stream(stream))
+    _check(st, "hswa_decode_multi")
 
 
 def decode(layer: Layer, shape: Shape, cache: Cache, q, context_lens, max_context_len: int, out,

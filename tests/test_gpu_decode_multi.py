@@ -1,0 +1,92 @@
+"""GPU parity of multi-query decode (hswa_decode_multi, the verification shape
+of multi-token prediction: several new tokens per sequence, causal among
+themselves) against the fp64 oracle: FULL layers with split-KV pieces whose
+last piece holds keys only the later queries see, SWA windows per query,
+GQA groups 1 to 16, and agreement with single-query decode."""
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import attention as OA
+from paper_2607_13095_amd import hswa
+from tests.hswa_testlib import SeqHistory, append_history, assert_close, i32, make_layer, to_dev, to_f64
+
+pytestmark = pytest.mark.gpu
+
+D = 128
+
+
+def run_multi(kind, window, pg, hq, hkv, ctxs, nq, seed, ctx_override=None):
+    """ctxs: cached tokens before the nq new ones; returns (gpu, ref) [ns, nq, hq, D]."""
+    ns = len(ctxs)
+    final = [c + nq for c in ctxs]
+    shape = hswa.Shape(hq, hkv, D, pg)
+    layer, kv = make_layer(kind, window, shape, final, seed)
+    hist = SeqHistory(final, hkv, D, *seed)
+    append_history(layer, shape, kv, hist, [0] * ns, ctxs)
+    append_history(layer, shape, kv, hist, ctxs, final)
+    qbits = synth.normal_bf16((ns, nq, hq, D), *seed, synth.TAG_QDEC)
+    lens = ctx_override if ctx_override is not None else final
+    maxc = max(max(lens), 1)
+    out = torch.full((ns, nq, hq, D), 7.0, dtype=torch.bfloat16, device="cuda")
+    wsb = hswa.decode_multi_workspace_bytes(shape, ns, nq, maxc)
+    ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device="cuda")
+    hswa.decode_multi(layer, shape, kv.cache, to_dev(qbits), i32(lens), maxc, out, workspace=ws)
+    torch.cuda.synchronize()
+    w = window if kind == "swa" else None
+    ref = np.zeros((ns, nq, hq, D))
+    for b in range(ns):
+        L = lens[b]
+        pos = np.arange(L - nq, L)
+        ok = pos >= 0
+        if ok.any():
+            ref[b][ok] = OA.masked_attention(OA.bf16_bits_to_f64(qbits[b][ok]), OA.bf16_bits_to_f64(hist.k[b][:L]),
+                                             OA.bf16_bits_to_f64(hist.v[b][:L]), pos[ok], w)
+    return to_f64(out), ref, (layer, shape, kv, qbits, lens, maxc)
+
+
+@pytest.mark.parametrize("nq", [2, 4, 7])
+@pytest.mark.parametrize("kind,window", [("full", 0), ("swa", 128), ("swa", 5), ("swa", 1)])
+def test_decode_multi(gpu_lib, nq, kind, window):
+    print(f"[decode-multi] nq={nq} {kind} W={window}", flush=True)
+    ctxs = [0, 1, 62, 63, 200, 1000, 3000]
+    gpu, ref, _ = run_multi(kind, window, 64, 64, 8, ctxs, nq, (900, nq, window))
+    assert_close(gpu, ref, f"decode multi nq={nq} {kind} W={window}")
+
+
+@pytest.mark.parametrize("hq,hkv", [(8, 8), (16, 1), (32, 4)])
+def test_decode_multi_groups(gpu_lib, hq, hkv):
+    print(f"[decode-multi-groups] hq={hq} hkv={hkv}", flush=True)
+    for kind, window in (("full", 0), ("swa", 128)):
+        gpu, ref, _ = run_multi(kind, window, 16, hq, hkv, [5, 300, 2500], 4, (901, hq, hkv))
+        assert_close(gpu, ref, f"decode multi groups {kind} hq={hq} hkv={hkv}")
+
+
+def test_decode_multi_split_tail(gpu_lib):
+    """FULL pieces: contexts (c + nq) one past a piece boundary, so the last
+    piece holds only the newest key, which the first three queries do not see."""
+    nq, ns, maxc = 4, 6, 6000
+    shape = hswa.Shape(64, 8, D, 64)
+    sl = hswa.decode_split_len(shape, ns, maxc)
+    ctxs = [sl + 1 - nq, 2 * sl + 1 - nq, 2 * sl + 2 - nq, sl - nq, 3 * sl + 3 - nq, maxc - nq]
+    gpu, ref, _ = run_multi("full", 0, 64, 64, 8, ctxs, nq, (902,))
+    assert_close(gpu, ref, f"decode multi split tail, split_len {sl}")
+
+
+def test_decode_multi_one_equals_decode(gpu_lib):
+    gpu, ref, (layer, shape, kv, qbits, lens, maxc) = run_multi("full", 0, 64, 64, 8, [100, 5000, 20000], 1, (903,))
+    assert_close(gpu, ref, "decode multi nq=1")
+    out = torch.empty((3, 64, D), dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(max(1, hswa.decode_workspace_bytes(shape, 3, maxc)), dtype=torch.uint8, device="cuda")
+    hswa.decode(layer, shape, kv.cache, to_dev(qbits[:, 0]), i32(lens), maxc, out, workspace=ws)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_f64(out), gpu[:, 0])
+
+
+def test_decode_multi_short_context_zero_rows(gpu_lib):
+    """context_lens below num_queries: queries at negative positions get zero rows."""
+    gpu, ref, _ = run_multi("full", 0, 16, 16, 2, [3, 3], 4, (904,), ctx_override=[2, 4])
+    assert np.all(gpu[0][:2] == 0) and np.all(gpu[0][2:] != 0)
+    assert_close(gpu, ref, "decode multi short")
