@@ -81,6 +81,7 @@ __device__ __forceinline__ int v_piece_keys(int tid, int i) { return 4 * i + (ti
 
 struct Stage {
   u32x4 k[kStage], v[kStage];
+  bool vrow;  // v[] holds 8 dims of one key (as k[]) instead of 8 keys of one dim
 };
 
 __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
@@ -192,6 +193,23 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
       }
       st.v[i] = v;
     }
+    st.vrow = false;
+  };
+  // Chunk tile: every key is one of this chunk's own (key >= P), so its K and
+  // V rows are 256-byte runs of k_new / v_new: both are loaded as 16-byte
+  // pieces of a key's row, and V is transposed on its way into LDS.
+  auto load_tile_chunk = [&](int kt, Stage &st) {
+#pragma unroll
+    for (int i = 0; i < kStage; ++i) {
+      const int idx = tid + kThreads * i;
+      const int j = kt + (idx >> 4);
+      const bool in = j >= klo && j <= khi;
+      const int64_t off = ((int64_t)(tok0 + (in ? j - P : 0)) * hkv + g) * kHeadDim + (idx & 15) * 8;
+      const u32x4 z = {0u, 0u, 0u, 0u};
+      st.k[i] = in ? ldg128(p.k_new + off) : z;
+      st.v[i] = in ? ldg128(p.v_new + off) : z;
+    }
+    st.vrow = true;
   };
   // Interior tile: every key cached, in range and (PG >= 64) on one page whose
   // id was fetched ahead; the K tile is 16 KiB and the V tile two [D][32]
@@ -208,6 +226,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
       st.k[i] = ldg128(kbase + (idx >> 4) * kHeadDim + (idx & 15) * 8);
       st.v[i] = ldg128(vbase + i * (32 * kHeadDim) + tid * 8);
     }
+    st.vrow = false;
   };
   // LDS addresses are a per-lane byte offset (fixed for the kernel) plus the
   // buffer's byte offset (a scalar), with everything else in the instruction's
@@ -216,14 +235,25 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   auto lds128 = [&](uint32_t off) { return reinterpret_cast<u32x4 *>(s_lds + off); };
   const uint32_t st_k0 = (k_lds_row(tid >> 4) * kKRow + (tid & 15) * 8) * 2;  // piece 0; piece 1 is 32 rows on
   const uint32_t st_v0 = kKTileBytes + (v_piece_dim(tid) * kVRow + v_piece_keys(tid, 0) * 8) * 2;
+  const uint32_t st_vrow0 = kKTileBytes + ((tid & 15) * 8 * kVRow + (tid >> 4)) * 2;  // row form, piece 0
   auto store_tile = [&](int buf, const Stage &st) {
     static_assert(kStage == 2, "two pieces per thread");
     const uint32_t bo = buf_off(buf);
     // piece 1 of K is key + 32 (LDS row + 32), of V keys + 32 (block 1)
     *lds128(bo + st_k0) = st.k[0];
     *lds128(bo + st_k0 + 32 * kKRow * 2) = st.k[1];
-    *lds128(bo + st_v0) = st.v[0];
-    *lds128(bo + st_v0 + 32 * 2) = st.v[1];
+    if (!st.vrow) {
+      *lds128(bo + st_v0) = st.v[0];
+      *lds128(bo + st_v0 + 32 * 2) = st.v[1];
+    } else {
+      // dims 8c .. 8c+7 of key tid/16 (+32 for piece 1): one 2-byte store per dim
+#pragma unroll
+      for (int i = 0; i < kStage; ++i)
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          *reinterpret_cast<uint16_t *>(s_lds + bo + st_vrow0 + (e * kVRow + 32 * i) * 2) =
+              (uint16_t)(st.v[i][e >> 1] >> (16 * (e & 1)));
+    }
   };
 
   float m[kCG], lsum[kCG];
@@ -274,6 +304,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   };
   auto fetch = [&](int kt, int page, Stage &st) {
     if (page >= 0) load_tile_page(kt, page, st);
+    else if (kt >= P) load_tile_chunk(kt, st);
     else load_tile(kt, st);
   };
 
