@@ -145,7 +145,18 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   }
 
   // ---- staging: global -> registers -> LDS ----
-  auto load_tile = [&](int kt, Stage &st) {
+  const bool page_tiles = shift >= 6;  // PG >= 64: a 64-key tile lies on one page
+  // General tile (range ends, the prefix / chunk boundary, PG < 64): per-key
+  // source and range checks. With PG >= 64 the tile's page (tpage, from the
+  // lane table) serves every cached key; otherwise each key looks its page up.
+  auto cached_page = [&](int j, int tpage, bool &ok) -> int64_t {
+    if (page_tiles) {
+      ok = tpage >= 0;
+      return ok ? tpage : 0;
+    }
+    return prefix_page(pv, b, j, ok);
+  };
+  auto load_tile = [&](int kt, int tpage, Stage &st) {
 #pragma unroll
     for (int i = 0; i < kStage; ++i) {
       const int idx = tid + kThreads * i;
@@ -155,7 +166,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
       if (j >= klo && j <= khi) {
         if (j < P) {
           bool ok;
-          const int64_t page = prefix_page(pv, b, j, ok);
+          const int64_t page = cached_page(j, tpage, ok);
           if (ok) v = ldg128(pv.k_pool + (((page * hkv + g) << shift) + (j & (pg - 1))) * kHeadDim + c * 8);
         } else {
           v = ldg128(p.k_new + ((int64_t)(tok0 + j - P) * hkv + g) * kHeadDim + c * 8);
@@ -170,7 +181,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
       u32x4 v = {0u, 0u, 0u, 0u};
       if (j0 >= klo && j0 + 7 <= khi && j0 + 7 < P) {
         bool ok;
-        const int64_t page = prefix_page(pv, b, j0, ok);
+        const int64_t page = cached_page(j0, tpage, ok);
         if (ok) v = ldg128(pv.v_pool + v_offset(pv, page, hkv, g, j0 & (pg - 1), d));
       } else if (j0 + 7 >= klo && j0 <= khi) {
         uint32_t e[8];
@@ -181,7 +192,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
           if (j >= klo && j <= khi) {
             if (j < P) {
               bool ok;
-              const int64_t page = prefix_page(pv, b, j, ok);
+              const int64_t page = cached_page(j, tpage, ok);
               if (ok) e[t] = pv.v_pool[v_offset(pv, page, hkv, g, j & (pg - 1), d)];
             } else {
               e[t] = p.v_new[((int64_t)(tok0 + j - P) * hkv + g) * kHeadDim + d];
@@ -275,7 +286,6 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   // and the one being written), with one barrier per tile.
   const int kt0 = klo & ~(kKT - 1);
   const int ntiles = (khi - kt0) / kKT + 1;
-  const bool page_tiles = shift >= 6;
   // A tile is "interior" when all of its keys are cached, inside [klo, khi]
   // and (PG >= 64) on a single page; its page id is looked up one tile ahead.
   auto interior = [&](int kt) { return page_tiles && kt >= klo && kt + kKT - 1 <= khi && kt + kKT - 1 < P; };
@@ -284,8 +294,11 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   // 64 pages, and a tile's id is read with v_readlane (no per-tile memory
   // round trip). -1 marks a tile that is not interior or whose page is invalid.
   int tab_page = -1, tab_lp0 = -(1 << 30);
+  // For PG >= 64 every 64-key tile lies on one logical page: its physical page
+  // comes from the lane table for any tile that starts in the cached prefix
+  // (-1 for a chunk tile or a page that is not valid).
   auto tile_page = [&](int kt) {
-    if (!interior(kt)) return -1;
+    if (!page_tiles || kt >= P) return -1;
     const int lp = kt >> shift;
     if (lp - tab_lp0 >= kWave || lp < tab_lp0) {
       tab_lp0 = lp;
@@ -303,9 +316,9 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
     return __builtin_amdgcn_readlane(tab_page, lp - tab_lp0);
   };
   auto fetch = [&](int kt, int page, Stage &st) {
-    if (page >= 0) load_tile_page(kt, page, st);
+    if (page >= 0 && interior(kt)) load_tile_page(kt, page, st);
     else if (kt >= P) load_tile_chunk(kt, st);
-    else load_tile(kt, st);
+    else load_tile(kt, page, st);
   };
 
   // QK^T of one half tile: S^T for keys kt + 32h .. +31.
