@@ -347,7 +347,7 @@ def allocator_report(wl, reps=20):
     for b in range(ns):
         assert alloc.admit(b, int(ctx[b]), 1) == 0 and alloc.extend(b, int(ctx[b])) == 0
     _, swa_tab = alloc.tables()
-    kp = torch.full((swa_pages, hkv, pg, d), float("nan"), dtype=torch.bfloat16, device="cuda")
+    kp = torch.full(hswa.k_pool_shape(swa_pages, hkv, pg, d), float("nan"), dtype=torch.bfloat16, device="cuda")
     vp = torch.full(hswa.v_pool_shape(swa_pages, hkv, pg, d), float("nan"), dtype=torch.bfloat16, device="cuda")
     cache = hswa.Cache(kp, vp, torch.from_numpy(swa_tab).cuda())
     i32 = lambda x: torch.as_tensor(np.asarray(x, dtype=np.int32), device="cuda")  # noqa: E731

@@ -34,13 +34,20 @@
  * Dtypes. q, k, v, out and the pools hold bf16 (raw 16-bit patterns). Scores,
  *   softmax and accumulation are fp32; outputs are rounded to bf16 with
  *   round-to-nearest-even.
- * Layout. Per layer there is one K pool and one V pool of `num_pages` pages:
- *     K pool: bf16 [num_pages][Hkv][page_size][head_dim]      (a row per token)
- *     V pool: bf16 [num_pages][Hkv][page_size/VB][head_dim][VB], VB = min(page_size, 32)
- *             (the keys of a page in blocks of VB, each block transposed, so
- *             the V^T of 32 consecutive keys of one head is one 8 KiB run)
- *   Slot s addresses page s / page_size at in-page offset o = s % page_size;
- *   its V values sit in block o / VB, column o % VB.
+ * Layout. Per layer there is one K pool and one V pool of `num_pages` pages;
+ *   both hold a page-head (one page of one KV head) as blocks of
+ *   B = min(page_size, 32) consecutive keys:
+ *     K pool: bf16 [num_pages][Hkv][page_size/B][2][head_dim/32][4][B/2][8]
+ *             key k of a block (k = o % B) sits in half (k / 4) % 2 at row
+ *             4 * (k / 8) + k % 4; its dim d in slab d / 32, piece (d / 8) % 4,
+ *             element d % 8. For B = 32 the 16 keys x 32 dims of one half and
+ *             slab (one QK^T operand of the bf16 matrix cores) are one
+ *             contiguous 1 KiB run in MFMA lane order.
+ *     V pool: bf16 [num_pages][Hkv][page_size/B][head_dim][B]
+ *             (each block transposed, so the V^T of 32 consecutive keys of one
+ *             head is one 8 KiB run)
+ *   Slot s addresses page s / page_size at in-page offset o = s % page_size,
+ *   block o / B; its V values sit in that block's column o % B.
  *   Every pool offset is computed in 64-bit.
  * Block tables (int32, device, row stride `table_stride`):
  *     FULL layer: table[b][i] = physical page of logical page i (positions
@@ -113,8 +120,8 @@ typedef struct {
 
 /* One layer's pool pair and its block table (see Layout / Block tables). */
 typedef struct {
-  void *k_pool;               /* device, bf16 [num_pages][Hkv][PG][D]          */
-  void *v_pool;               /* device, bf16 [num_pages][Hkv][PG/VB][D][VB]   */
+  void *k_pool;               /* device, bf16 [num_pages][Hkv][PG/B][2][D/32][4][B/2][8] */
+  void *v_pool;               /* device, bf16 [num_pages][Hkv][PG/B][D][B]               */
   int64_t num_pages;
   const int32_t *block_table; /* device, int32 [ns][table_stride]              */
   int32_t table_stride;

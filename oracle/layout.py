@@ -21,10 +21,12 @@ Readings where the paper is silent:
     with n_b = ceil(L_b_final / PG) for FULL and n_b = R for SWA.
 
 Pool layout (one pool per layer and per K / V; the paper fixes none, this is
-the library's own):
-  K pool: [num_pages][Hkv][PG][D]          (key-major rows inside a page)
-  V pool: [num_pages][Hkv][PG/VB][D][VB]   (blocks of VB = min(PG, 32) keys,
-                                             each transposed)
+the library's own). Both pools hold a page-head as blocks of B = min(PG, 32)
+consecutive keys:
+  K pool: [num_pages][Hkv][PG/B][2][D/32][4][B/2][8]
+          key k of a block sits in half (k // 4) % 2 at row 4 (k // 8) + k % 4;
+          dim d in 32-dim slab d // 32, 8-dim piece (d // 8) % 4, element d % 8
+  V pool: [num_pages][Hkv][PG/B][D][B]     (each block transposed)
 A slot s addresses page s // PG, in-page offset s % PG.
 """
 
@@ -98,25 +100,60 @@ def slot_mapping(kind, window, page_size, table, start_pos, new_lens) -> np.ndar
     return np.asarray(out, dtype=np.int64)
 
 
+def key_block(page_size: int) -> int:
+    """Keys per block of both pools: B = min(PG, 32)."""
+    return min(int(page_size), 32)
+
+
+def k_pool_shape(num_pages: int, num_kv_heads: int, page_size: int, head_dim: int):
+    """[num_pages][Hkv][PG/B][2][D/32][4][B/2][8] (see the module header)."""
+    b = key_block(page_size)
+    if b < 8 or int(page_size) % b or int(head_dim) % 32:
+        raise ValueError("the K layout needs PG >= 8 and head_dim a multiple of 32")
+    return (int(num_pages), int(num_kv_heads), int(page_size) // b, 2, int(head_dim) // 32, 4, b // 2, 8)
+
+
+def k_slot(k_pool_shape_, page: int, off: int):
+    """Index (for numpy or torch) of the Hkv x D values of in-page offset
+    `off` of `page` in a K pool of the given shape; the selection has shape
+    [Hkv][D/32][4][8], i.e. the key's dims in order after a reshape to
+    [Hkv][D]."""
+    b = 2 * int(k_pool_shape_[6])
+    k = int(off) % b
+    half, row = (k // 4) % 2, 4 * (k // 8) + k % 4
+    return (int(page), slice(None), int(off) // b, half, slice(None), slice(None), row, slice(None))
+
+
+def k_rows(k_pool, page: int, off: int):
+    """The [Hkv][D] K values stored for in-page offset `off` of `page`."""
+    sel = k_pool[k_slot(k_pool.shape, page, off)]
+    return sel.reshape(sel.shape[0], -1)
+
+
 def apply_append(k_pool, v_pool, slots, k_new, v_new):
     """Expected pool content after an append (copies; bf16 bits as uint16).
 
-    k_pool: [P][Hkv][PG][D] (one row per slot). v_pool: [P][Hkv][PG/VB][D][VB]:
-    the keys of a page in blocks of VB = min(PG, 32), each block stored with
-    the dim index outer. k_new, v_new: [T][Hkv][D]. Tokens whose slot is -1 are
-    not stored.
+    k_pool: [P][Hkv][PG/B][2][D/32][4][B/2][8]; v_pool: [P][Hkv][PG/B][D][B]
+    (B = min(PG, 32); the module header gives the element order). k_new,
+    v_new: [T][Hkv][D]. Tokens whose slot is -1 are not stored.
     """
     k_pool = np.array(k_pool, copy=True)
     v_pool = np.array(v_pool, copy=True)
-    pg = k_pool.shape[2]
+    if k_pool.ndim != 8 or v_pool.ndim != 5:
+        raise ValueError("k_pool is 8-D and v_pool 5-D")
+    npg, hkv = k_pool.shape[:2]
+    pg = k_pool.shape[2] * 2 * k_pool.shape[6]
+    d = k_pool.shape[4] * 32
+    if tuple(k_pool.shape) != k_pool_shape(npg, hkv, pg, d):
+        raise ValueError("k_pool must be [P][Hkv][PG/B][2][D/32][4][B/2][8]")
     vb = v_pool.shape[4]
-    if vb != min(pg, 32) or v_pool.shape[2] * vb != pg:
+    if vb != key_block(pg) or v_pool.shape[2] * vb != pg:
         raise ValueError("v_pool blocks must hold min(PG, 32) keys")
     for t, s in enumerate(np.asarray(slots)):
         if s < 0:
             continue
         page, off = int(s) // pg, int(s) % pg
-        k_pool[page, :, off, :] = k_new[t]
+        k_pool[k_slot(k_pool.shape, page, off)] = np.asarray(k_new[t]).reshape(hkv, d // 32, 4, 8)
         v_pool[page, :, off // vb, :, off % vb] = v_new[t]
     return k_pool, v_pool
 

@@ -1,4 +1,4 @@
-// Decode attention over the paged KV cache (one query per sequence).
+// Decode attention over the paged KV cache (one or a few queries per sequence).
 //
 // "KVCache Storage Analysis": decode is memory-bound, its cost follows the KV
 // bytes read; SWA layers read at most W keys from the per-sequence ring, FULL
@@ -7,30 +7,42 @@
 // Work item: one wavefront per (sequence, KV head, group of up to 16 query heads
 // of that KV head, key range). An SWA layer (or a FULL layer short enough for
 // one piece) has one item per (sequence, head group) covering every visible key;
-// a FULL layer splits the context into pieces of split_len keys. Workgroups are
-// single waves, one item each; split items are numbered over the pieces that
-// exist, so the dispatcher balances the uneven sequence lengths by itself.
+// a FULL layer splits the context into pieces of split_len keys. A workgroup
+// holds four waves (split pieces) or one, each wave with an item of its own (no
+// LDS, no barrier); split items are numbered over the pieces that exist, so
+// the dispatcher balances the uneven sequence lengths by itself.
 //
 // Per item the wave walks 32-key chunks and runs both products on the bf16
 // matrix cores with the GQA query heads as the 16 MFMA columns:
-//   S^T[key][head]  = K[key][:] . Q[head][:]        (K rows straight from HBM)
+//   S^T[key][head]  = K[key][:] . Q[head][:]        (K slabs straight from HBM)
 //   O^T[d][head]   += V^T[d][key] . P^T[key][head]   (V pages hold [D][32] blocks)
 // The 32 keys of a chunk are assigned to MFMA rows so that the score tile comes
 // out with each lane holding 8 consecutive keys of one head, which is exactly
-// the lane layout the PV product needs for P^T: no shuffle between the two.
+// the lane layout the PV product needs for P^T: no shuffle between the two; the
+// K pool stores each 32-key block in that row order, so every K load
+// instruction reads one contiguous 1 KiB (and every V load as well).
 // Softmax is online per chunk in fp32 (exp2 with scale*log2(e) folded in).
 // The K loads of chunk c+1 are in flight while chunk c's softmax and PV run,
 // its V loads while chunk c+1's QK^T runs. A split item writes fp32 (o, log2
 // sum-exp) partials that a second kernel merges; a whole-range item writes bf16.
+#include <cfloat>
+
 #include "hswa_common.h"
 #include "hswa_launch.h"
 
 namespace hswa {
 namespace {
 
+// KV bytes are read once per call: non-temporal loads keep them from
+// displacing reusable lines in L2 and the memory-side cache.
+__device__ __forceinline__ u32x4 ldnt128(const void *p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+}
+
 constexpr int kChunk = 32;
 constexpr int kCols = 16;  // query heads per item (MFMA columns)
 constexpr int kMergeThreads = 256;
+constexpr float kRescaleLog2 = 8.f;  // lazy raise threshold of the running maximum (exp2 units)
 
 // Per-wave copy of a window of the block table: lane i holds the physical page
 // of logical page lp0 + i (-1 if outside the range or not a valid page id), so
@@ -60,10 +72,19 @@ struct Chunk {
   bool vok;
 };
 
+// Waves (independent items) per workgroup: four for split pieces (thousands of
+// items), one for whole ranges (an SWA layer has only sequences x head groups
+// items, which four-wave workgroups would spread over too few CUs).
+template <bool kSplit>
+constexpr int kWaves = kSplit ? 4 : 1;
+
+// At most 168 VGPRs, so that three waves share a SIMD.
 template <bool kSplit, bool kOnePage>
-__global__ __launch_bounds__(kWave) void decode_kernel(DecodeParams p) {
+__global__ __launch_bounds__(kWave * kWaves<kSplit>) __attribute__((amdgpu_waves_per_eu(3))) void decode_kernel(
+    DecodeParams p) {
   const PoolView &pv = p.pool;
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t item = (int64_t)blockIdx.x * kWaves<kSplit> + (threadIdx.x >> 6);
   const int r = lane & 15, q = lane >> 4;
   const int hkv = p.hkv;
   const int shift = pv.pg_shift;
@@ -72,10 +93,12 @@ __global__ __launch_bounds__(kWave) void decode_kernel(DecodeParams p) {
   const int ncols = p.nq * p.group;  // (query, head) pairs of one KV head
   const int hchunks = (ncols + kCols - 1) / kCols;
 
-  // Loop-invariant byte offsets of this lane's operands inside one page-head
-  // (used when a 32-key chunk never straddles two pages, i.e. PG >= 32).
-  const uint32_t koff_a = ((8 * (r >> 2) + (r & 3)) * kHeadDim + 8 * q) * 2;
-  const uint32_t koff_b = koff_a + 4 * kHeadDim * 2;
+  // Loop-invariant byte offsets of this lane's operands inside one 32-key K
+  // block (used when a 32-key chunk never straddles two pages, i.e. PG >= 32):
+  // slab t of half a (keys 8i + j, j < 4: MFMA rows 4i + j) is the A operand
+  // of step t in lane order, a contiguous 1 KiB; half b (keys 8i + 4 + j) 4 KiB on.
+  const uint32_t koff_a = lane * 16;
+  const uint32_t koff_b = koff_a + 4096;
   // V^T of a 32-key chunk is one [D][32] block when PG >= 32: lane reads dims
   // 16 dt + r, keys 8 q .. 8 q + 7 of it.
   const uint32_t voff = (r * 32 + 8 * q) * 2;
@@ -86,10 +109,10 @@ __global__ __launch_bounds__(kWave) void decode_kernel(DecodeParams p) {
   // every launched workgroup up to the real item count has work and the
   // surplus of the upper-bound grid exits at once.
   const int H = hkv * hchunks;
-  const int gy = (int)(blockIdx.x % H);
+  const int gy = (int)(item % H);
   int b = 0, split = 0;
   if constexpr (kSplit) {
-    const int64_t j = blockIdx.x / H;  // index of the (sequence, piece) pair
+    const int64_t j = item / H;  // index of the (sequence, piece) pair
     int64_t base = 0;
     b = -1;
     for (int b0 = 0; b0 < p.ns; b0 += kWave) {
@@ -118,7 +141,8 @@ __global__ __launch_bounds__(kWave) void decode_kernel(DecodeParams p) {
     }
     if (b < 0) return;
   } else {
-    b = (int)(blockIdx.x / H);
+    if (item >= (int64_t)p.ns * H) return;
+    b = (int)(item / H);
   }
   {
     const int g = gy / hchunks;
@@ -174,7 +198,9 @@ __global__ __launch_bounds__(kWave) void decode_kernel(DecodeParams p) {
     LaneTable tab;
     load_lane_table(tab, pv, b, kb >> shift, last_lp, lane);
 
-    float m = -INFINITY, lsum = 0.f;
+    // Running column maximum: finite start, raised lazily (see scores).
+    float m = -FLT_MAX, lsum = 0.f;
+    const float thresh = kRescaleLog2 / c2;  // in raw score units
     f32x4 acc[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -186,8 +212,8 @@ __global__ __launch_bounds__(kWave) void decode_kernel(DecodeParams p) {
                           ((((pg64 * hkv + g) << shift) + (cbase & (pg - 1))) * kHeadDim) * 2;
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        ch.ka[t] = ldg128(kbase + koff_a + 64 * t);
-        ch.kb[t] = ldg128(kbase + koff_b + 64 * t);
+        ch.ka[t] = ldnt128(kbase + koff_a + 1024 * t);
+        ch.kb[t] = ldnt128(kbase + koff_b + 1024 * t);
       }
     };
     auto issue_v = [&](int c, int page, Chunk &ch) {
@@ -200,7 +226,7 @@ __global__ __launch_bounds__(kWave) void decode_kernel(DecodeParams p) {
       ch.kv0 = cbase + 8 * q;
       ch.vok = page >= 0;
 #pragma unroll
-      for (int dt = 0; dt < 8; ++dt) ch.v[dt] = ldg128(vbase + voff + dt * vstep);
+      for (int dt = 0; dt < 8; ++dt) ch.v[dt] = ldnt128(vbase + voff + dt * vstep);
     };
     // General path (PG = 16: a chunk spans two pages): per-lane page choice.
     auto issue = [&](int c, Chunk &ch) {
@@ -219,21 +245,28 @@ __global__ __launch_bounds__(kWave) void decode_kernel(DecodeParams p) {
       ch.kv0 = cbase + 8 * q;
       ch.vok = pvv >= 0;
       const int64_t pa64 = max(pa, 0), pb64 = max(pb, 0), pv64 = max(pvv, 0);
-      const uint16_t *krow_a = pv.k_pool + (((pa64 * hkv + g) << shift) + (ka & (pg - 1))) * kHeadDim;
-      const uint16_t *krow_b = pv.k_pool + (((pb64 * hkv + g) << shift) + (kb2 & (pg - 1))) * kHeadDim;
+      // dims 32 t + 8 q .. +7 of a key: slab t of its half, 16 * B elements apart
+      const int64_t kstep = (int64_t)16 << pv.vb_shift;
+      const uint16_t *krow_a = pv.k_pool + k_offset(pv, pa64, hkv, g, ka & (pg - 1), 8 * q);
+      const uint16_t *krow_b = pv.k_pool + k_offset(pv, pb64, hkv, g, kb2 & (pg - 1), 8 * q);
       const uint16_t *vcol = pv.v_pool + v_offset(pv, pv64, hkv, g, kvg & (pg - 1), r);
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
-        ch.ka[t] = ldg128(krow_a + 32 * t + 8 * q);
-        ch.kb[t] = ldg128(krow_b + 32 * t + 8 * q);
+        ch.ka[t] = ldnt128(krow_a + kstep * t);
+        ch.kb[t] = ldnt128(krow_b + kstep * t);
       }
 #pragma unroll
-      for (int dt = 0; dt < 8; ++dt) ch.v[dt] = ldg128(vcol + ((int64_t)(16 * dt) << pv.vb_shift));
+      for (int dt = 0; dt < 8; ++dt) ch.v[dt] = ldnt128(vcol + ((int64_t)(16 * dt) << pv.vb_shift));
     };
 
     // QK^T and the online softmax of one chunk: returns P^T packed as bf16 and
-    // leaves the rescale factor in `alpha` and the key mask in `keep`.
-    float alpha = 1.f;
+    // leaves the key mask in `keep`. The running maximum of a column is only
+    // raised when one of its scores exceeds it by more than 2^8 in exp2 units
+    // (a ballot over the lanes' own maxima; the exact column maximum is formed
+    // only then), so the output rescale is rare; numerator and denominator
+    // share the stale maximum, so the result is exact. Starting from -FLT_MAX,
+    // a masked score (-inf) gives probability 0 without (-inf) - (-inf), and
+    // the first finite score always raises the maximum (alpha = 0).
     uint32_t keep = 0;
     auto scores = [&](Chunk &ch) {
       f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
@@ -259,21 +292,25 @@ __global__ __launch_bounds__(kWave) void decode_kernel(DecodeParams p) {
         s[i] = (sk >> i) & 1u ? sa[i] : -INFINITY;
         s[4 + i] = (sk >> (4 + i)) & 1u ? sb[i] : -INFINITY;
       }
-      const float cmax = max_xor32(max_xor16(max8(s)));
-      const float mnew = fmaxf(m, cmax);
-      const float mc = mnew == -INFINITY ? 0.f : mnew * c2;
-      alpha = fast_exp2(m * c2 - mc);
-      float pr[8], psum = 0.f;
+      const float lmax = max8(s);
+      if (__builtin_amdgcn_ballot_w64(lmax > m + thresh) != 0) {
+        const float cmax = max_xor32(max_xor16(lmax));
+        const bool up = cmax > m + thresh;
+        const float alpha = up ? fast_exp2((m - cmax) * c2) : 1.f;
+        m = up ? cmax : m;
+        lsum *= alpha;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        pr[i] = fast_exp2(fmaf(s[i], c2, -mc));
-        psum += pr[i];
+        for (int dt = 0; dt < 8; ++dt) acc[dt] *= alpha;
       }
-      lsum = lsum * alpha + psum;
-      m = mnew;
+      const float mc = m * c2;
+      float pr[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) pr[i] = fast_exp2(fmaf(s[i], c2, -mc));
       u32x4 pf;
 #pragma unroll
       for (int j = 0; j < 4; ++j) pf[j] = pack_bf16x2(pr[2 * j], pr[2 * j + 1]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) lsum = dot2_bf16_ones(pf[j], lsum);
       return pf;
     };
     auto pv_update = [&](Chunk &ch, u32x4 pf) {
@@ -282,17 +319,12 @@ __global__ __launch_bounds__(kWave) void decode_kernel(DecodeParams p) {
         for (int dt = 0; dt < 8; ++dt) ch.v[dt] = keep_bf16x8(ch.v[dt], keep);
       }
 #pragma unroll
-      for (int dt = 0; dt < 8; ++dt) {
-        acc[dt] *= alpha;
-        acc[dt] = mfma16x16x32(ch.v[dt], pf, acc[dt]);
-      }
+      for (int dt = 0; dt < 8; ++dt) acc[dt] = mfma16x16x32(ch.v[dt], pf, acc[dt]);
     };
 
     // The one-page path needs every page of the range in the lane table; the
     // host only selects it when every range spans fewer than 64 pages.
     if constexpr (kOnePage) {
-      // Rolling prefetch with one register set; the last chunk is peeled so
-      // that the loop body always prefetches (uniform wait counts).
       auto page_of = [&](int c) {
         return __builtin_amdgcn_readlane(tab.page, ((cfirst + c * kChunk) >> shift) - tab.lp0);
       };
@@ -302,12 +334,18 @@ __global__ __launch_bounds__(kWave) void decode_kernel(DecodeParams p) {
         issue_k(0, page, ch);
         issue_v(0, page, ch);
       }
+      // The scheduling fences keep each chunk's loads behind the last use of
+      // the registers they overwrite: one operand set, no loop-carried copies.
       for (int c = 0; c < nchunks - 1; ++c) {
         const int next_page = page_of(c + 1);
         const u32x4 pf = scores(ch);
+        __builtin_amdgcn_sched_barrier(0);
         issue_k(c + 1, next_page, ch);
+        __builtin_amdgcn_sched_barrier(0);
         pv_update(ch, pf);
+        __builtin_amdgcn_sched_barrier(0);
         issue_v(c + 1, next_page, ch);
+        __builtin_amdgcn_sched_barrier(0);
       }
       const u32x4 pf = scores(ch);
       pv_update(ch, pf);
@@ -366,6 +404,10 @@ __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(DecodeParam
 #pragma unroll
   for (int off = 8; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, kWave));
   mx = max_xor32(max_xor16(mx));
+  if (mx == -INFINITY) {  // a query that sees no key (multi-query rows before position 0)
+    *dst = 0u;
+    return;
+  }
   const float *po = p.ws_o + idx * p.max_splits * kHeadDim + 2 * lane;
   float wsum = 0.f, o0 = 0.f, o1 = 0.f;
   for (int s0 = 0; s0 < nsplit; s0 += kWave) {
@@ -413,7 +455,8 @@ hipError_t launch_decode(const DecodeParams &p, hipStream_t stream) {
   if (p.ns <= 0) return hipSuccess;
   const int hchunks = (p.nq * p.group + kCols - 1) / kCols;
   const int64_t items = (int64_t)p.ns * p.hkv * hchunks * p.max_splits;  // upper bound
-  const unsigned grid = (unsigned)items;
+  const unsigned grid4 = (unsigned)((items + kWaves<true> - 1) / kWaves<true>);
+  const unsigned grid1 = (unsigned)items;
   // One-page path: 32-key chunks never straddle pages (PG >= 32) and every key
   // range fits the 64-entry lane table.
   const int64_t range = p.max_splits > 1 ? p.split_len
@@ -421,16 +464,18 @@ hipError_t launch_decode(const DecodeParams &p, hipStream_t stream) {
   const int64_t range_pages = ((range + (1 << p.pool.pg_shift) - 1) >> p.pool.pg_shift) + 1;
   const bool one_page = p.pool.pg_shift >= 5 && range_pages < kWave;
   if (p.max_splits > 1) {
-    const hipError_t e = one_page ? launch_kernel(decode_kernel<true, true>, dim3(grid), dim3(kWave), stream, p)
-                                  : launch_kernel(decode_kernel<true, false>, dim3(grid), dim3(kWave), stream, p);
+    const dim3 block(kWave * kWaves<true>);
+    const hipError_t e = one_page ? launch_kernel(decode_kernel<true, true>, dim3(grid4), block, stream, p)
+                                  : launch_kernel(decode_kernel<true, false>, dim3(grid4), block, stream, p);
     if (e != hipSuccess) return e;
     const int64_t rows = (int64_t)p.ns * p.nq * p.hq;
     const int per_block = kMergeThreads / kWave;
     return launch_kernel(decode_merge_kernel, dim3((unsigned)((rows + per_block - 1) / per_block)),
                          dim3(kMergeThreads), stream, p);
   }
-  return one_page ? launch_kernel(decode_kernel<false, true>, dim3(grid), dim3(kWave), stream, p)
-                  : launch_kernel(decode_kernel<false, false>, dim3(grid), dim3(kWave), stream, p);
+  const dim3 block(kWave * kWaves<false>);
+  return one_page ? launch_kernel(decode_kernel<false, true>, dim3(grid1), block, stream, p)
+                  : launch_kernel(decode_kernel<false, false>, dim3(grid1), block, stream, p);
 }
 
 }  // namespace hswa

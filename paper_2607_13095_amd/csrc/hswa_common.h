@@ -31,6 +31,20 @@ __device__ __forceinline__ u32x4 ldg128(const void *p) {
 
 __device__ __forceinline__ void stg128(void *p, u32x4 v) { *reinterpret_cast<u32x4 *>(p) = v; }
 
+// Element offset in the K pool of (page, KV head g, in-page key offset o, dim d).
+// In a block of B = 2^vb_shift keys, key k sits in half (k >> 2) & 1 at row
+// ((k >> 3) << 2) | (k & 3); dim d in slab d >> 5, 16-byte piece (d >> 3) & 3.
+// A slab is [4 pieces][B/2 rows][8 dims], so for B = 32 the bf16-MFMA A operand
+// of 16 keys (lane = row + 16 * piece) x 32 dims is lane-linear.
+__device__ __forceinline__ int64_t k_offset(const PoolView &pv, int64_t page, int hkv, int g, int o, int d) {
+  const int kb = pv.vb_shift;
+  const int k = o & ((1 << kb) - 1);
+  const int half = (k >> 2) & 1, row = ((k >> 3) << 2) | (k & 3);
+  const int slab = (half << 2) | (d >> 5);
+  return (((page * hkv + g) << pv.pg_shift) << kHeadDimShift) + ((int64_t)(o >> kb) << (kb + kHeadDimShift)) +
+         ((((slab << 2) | ((d >> 3) & 3)) << (kb - 1)) + row) * 8 + (d & 7);
+}
+
 // Element offset in the V pool of (page, KV head g, in-page key offset o, dim d).
 __device__ __forceinline__ int64_t v_offset(const PoolView &pv, int64_t page, int hkv, int g, int o, int d) {
   const int vb = pv.vb_shift;

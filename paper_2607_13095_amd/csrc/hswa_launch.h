@@ -9,20 +9,23 @@ namespace hswa {
 
 constexpr int kHeadDim = 128;  // the only head dim the kernels are built for
 constexpr int kHeadDimShift = 7;
-// V pages are stored as PG / VB blocks of VB = min(PG, 32) consecutive keys,
-// each block transposed ([D][VB]): the V^T operand of a 32-key chunk of one
-// head is one contiguous 8 KiB run.
+// Both pools store a page-head as PG / B blocks of B = min(PG, 32) consecutive
+// keys. V blocks are transposed ([D][B]): the V^T operand of a 32-key chunk of
+// one head is one contiguous 8 KiB run. K blocks hold two halves (keys whose
+// in-block offset has bit 2 clear, then set), each as four 32-dim slabs of
+// [B/2 keys][32 dims] with the 16-byte pieces in bf16-MFMA lane order: the 16
+// keys x 32 dims of one QK^T operand are one contiguous 1 KiB run (B = 32).
 constexpr int kVBlockShiftMax = 5;
 
 // Pool geometry and block table of one layer, as the kernels see it.
 struct PoolView {
-  uint16_t *k_pool;       // bf16 [num_pages][Hkv][PG][D]
-  uint16_t *v_pool;       // bf16 [num_pages][Hkv][PG/VB][D][VB]
+  uint16_t *k_pool;       // bf16 [num_pages][Hkv][PG/B][2][D/32][4][B/2][8]
+  uint16_t *v_pool;       // bf16 [num_pages][Hkv][PG/B][D][B]
   int64_t num_pages;
   const int32_t *table;   // int32 [ns][stride]
   int32_t stride;
   int32_t pg_shift;       // log2(page size)
-  int32_t vb_shift;       // log2(VB) = min(pg_shift, 5)
+  int32_t vb_shift;       // log2(B) = min(pg_shift, 5), the key block of both pools
   int32_t ring;           // ring pages R (SWA) or 0 (FULL)
   int32_t window;         // SWA window W, or 0 for FULL
 };

@@ -6,11 +6,11 @@
 // and every decode step ("SWA-Aware Prefix Cache Tree").
 //
 // One workgroup handles 8 consecutive tokens of the flattened batch for one KV
-// head. The K row of a token is one contiguous 256-byte run per KV head in the
-// pool; V pages are stored as transposed blocks of VB = min(PG, 32) keys
-// ([D][VB] per block and head), so 8 tokens that land on 8 consecutive,
-// 8-aligned slots of one page are written as one 16-byte store per dim;
-// anything else falls back to 2-byte stores.
+// head. A token's K row goes to the pool as sixteen 16-byte pieces (the K
+// blocks are stored in MFMA-operand slabs); V pages are stored as transposed
+// blocks of B = min(PG, 32) keys ([D][B] per block and head), so 8 tokens that
+// land on 8 consecutive, 8-aligned slots of one page are written as one 16-byte
+// store per dim; anything else falls back to 2-byte stores.
 #include "hswa_common.h"
 #include "hswa_launch.h"
 
@@ -71,14 +71,14 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(AppendParams p) {
   const int hkv = p.hkv;
   constexpr int kRow16 = kHeadDim / 8;  // 16-byte pieces per K row
 
-  // K rows: contiguous per (page, head, offset); threads 0..127 copy 8 rows.
+  // K rows: threads 0..127 copy the 16-byte pieces of 8 rows.
   if (tid < kTokPerBlock * kRow16) {
     const int tok = tid / kRow16, c = tid % kRow16;
     const int64_t s = tok < ntok ? s_slot[tok] : -1;
     if (s >= 0) {
       const int64_t page = s >> pv.pg_shift, off = s & (pg - 1);
       const u32x4 v = ldg128(p.k_new + ((int64_t)(t0 + tok) * hkv + g) * kHeadDim + c * 8);
-      stg128(pv.k_pool + ((page * hkv + g) * pg + off) * kHeadDim + c * 8, v);
+      stg128(pv.k_pool + k_offset(pv, page, hkv, g, (int)off, c * 8), v);
     }
   }
 

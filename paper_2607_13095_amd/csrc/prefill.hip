@@ -76,6 +76,17 @@ static_assert(kStage == 2 && kKT == 64, "V staging maps piece i of a thread to 3
 // V^T tile staging: piece i of thread tid holds dim tid / 4 and keys
 // 8 * (4 i + tid % 4) .. +7 of the tile, which in the pool is the 16 bytes at
 // element 8 * tid of the tile's 32-key block i.
+// K tile pieces in pool order: piece idx (0 .. 1023) is 16-byte piece idx & 511
+// of the tile's 32-key block idx >> 9 (half (idx >> 8) & 1, slab (idx >> 6) & 3,
+// dim piece (idx >> 4) & 3, row idx & 15 of the block's K layout), i.e. dims
+// 8 k_piece_c .. +7 of tile key k_piece_key, which LDS holds in row k_piece_row.
+__device__ __forceinline__ int k_piece_key(int idx) {
+  const int r = idx & 15;
+  return ((idx >> 9) << 5) | ((r >> 2) << 3) | (((idx >> 8) & 1) << 2) | (r & 3);
+}
+__device__ __forceinline__ int k_piece_c(int idx) { return ((idx >> 6) & 3) * 4 + ((idx >> 4) & 3); }
+__device__ __forceinline__ int k_piece_row(int idx) { return ((idx >> 8) << 4) | (idx & 15); }
+
 __device__ __forceinline__ int v_piece_dim(int tid) { return tid >> 2; }
 __device__ __forceinline__ int v_piece_keys(int tid, int i) { return 4 * i + (tid & 3); }
 
@@ -160,14 +171,14 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
 #pragma unroll
     for (int i = 0; i < kStage; ++i) {
       const int idx = tid + kThreads * i;
-      const int key = idx >> 4, c = idx & 15;
-      const int j = kt + key;
+      const int c = k_piece_c(idx);
+      const int j = kt + k_piece_key(idx);
       u32x4 v = {0u, 0u, 0u, 0u};
       if (j >= klo && j <= khi) {
         if (j < P) {
           bool ok;
           const int64_t page = cached_page(j, tpage, ok);
-          if (ok) v = ldg128(pv.k_pool + (((page * hkv + g) << shift) + (j & (pg - 1))) * kHeadDim + c * 8);
+          if (ok) v = ldg128(pv.k_pool + k_offset(pv, page, hkv, g, j & (pg - 1), c * 8));
         } else {
           v = ldg128(p.k_new + ((int64_t)(tok0 + j - P) * hkv + g) * kHeadDim + c * 8);
         }
@@ -223,18 +234,18 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
     st.vrow = true;
   };
   // Interior tile: every key cached, in range and (PG >= 64) on one page whose
-  // id was fetched ahead; the K tile is 16 KiB and the V tile two [D][32]
-  // blocks of 8 KiB, all contiguous: plain 16-byte loads, consecutive threads
-  // at consecutive addresses.
+  // id was fetched ahead; the K tile is two 8 KiB K blocks and the V tile two
+  // [D][32] blocks of 8 KiB, all contiguous: plain 16-byte loads, consecutive
+  // threads at consecutive addresses.
   auto load_tile_page = [&](int kt, int page, Stage &st) {
     const int64_t pg64 = max(page, 0);
     const int off = kt & (pg - 1);
-    const uint16_t *kbase = pv.k_pool + ((((pg64 * hkv + g) << shift) + off) * kHeadDim);
+    const uint16_t *kbase = pv.k_pool + k_offset(pv, pg64, hkv, g, off, 0);
     const uint16_t *vbase = pv.v_pool + v_offset(pv, pg64, hkv, g, off, 0);
 #pragma unroll
     for (int i = 0; i < kStage; ++i) {
       const int idx = tid + kThreads * i;
-      st.k[i] = ldg128(kbase + (idx >> 4) * kHeadDim + (idx & 15) * 8);
+      st.k[i] = ldg128(kbase + idx * 8);
       st.v[i] = ldg128(vbase + i * (32 * kHeadDim) + tid * 8);
     }
     st.vrow = false;
@@ -244,15 +255,19 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   // immediate offset field.
   auto buf_off = [&](int buf) { return (uint32_t)__builtin_amdgcn_readfirstlane(buf * kBufBytes); };
   auto lds128 = [&](uint32_t off) { return reinterpret_cast<u32x4 *>(s_lds + off); };
-  const uint32_t st_k0 = (k_lds_row(tid >> 4) * kKRow + (tid & 15) * 8) * 2;  // piece 0; piece 1 is 32 rows on
+  // K piece 0 of this thread in pool order (cached tiles) or row order (chunk
+  // tiles); piece 1 is 32 rows on in both.
+  const uint32_t st_k0 = (k_piece_row(tid) * kKRow + k_piece_c(tid) * 8) * 2;
+  const uint32_t st_k0_row = (k_lds_row(tid >> 4) * kKRow + (tid & 15) * 8) * 2;
   const uint32_t st_v0 = kKTileBytes + (v_piece_dim(tid) * kVRow + v_piece_keys(tid, 0) * 8) * 2;
   const uint32_t st_vrow0 = kKTileBytes + ((tid & 15) * 8 * kVRow + (tid >> 4)) * 2;  // row form, piece 0
   auto store_tile = [&](int buf, const Stage &st) {
     static_assert(kStage == 2, "two pieces per thread");
     const uint32_t bo = buf_off(buf);
     // piece 1 of K is key + 32 (LDS row + 32), of V keys + 32 (block 1)
-    *lds128(bo + st_k0) = st.k[0];
-    *lds128(bo + st_k0 + 32 * kKRow * 2) = st.k[1];
+    const uint32_t k0 = st.vrow ? st_k0_row : st_k0;
+    *lds128(bo + k0) = st.k[0];
+    *lds128(bo + k0 + 32 * kKRow * 2) = st.k[1];
     if (!st.vrow) {
       *lds128(bo + st_v0) = st.v[0];
       *lds128(bo + st_v0 + 32 * 2) = st.v[1];

@@ -197,19 +197,31 @@ def v_pool_shape(num_pages: int, num_kv_heads: int, page_size: int, head_dim: in
     return (int(num_pages), int(num_kv_heads), int(page_size) // vb, int(head_dim), vb)
 
 
+def k_pool_shape(num_pages: int, num_kv_heads: int, page_size: int, head_dim: int = 128):
+    """[num_pages, Hkv, PG/B, 2, D/32, 4, B/2, 8] with B = min(PG, 32): per block
+    of B keys, two halves (in-block offset bit 2 clear / set) of D/32 slabs of
+    [4 dim pieces][B/2 keys][8 dims] (the element order is in include/hswa.h)."""
+    b = v_block(page_size)
+    return (int(num_pages), int(num_kv_heads), int(page_size) // b, 2, int(head_dim) // 32, 4, b // 2, 8)
+
+
 class Cache:
     """One layer's K pool, V pool and block table (device tensors).
 
-    k_pool: bf16 [num_pages, Hkv, PG, D]; v_pool: bf16 [num_pages, Hkv, PG/VB, D, VB]
-    with VB = min(PG, 32) (see include/hswa.h); block_table: int32 [ns, stride].
+    k_pool: bf16 k_pool_shape(num_pages, Hkv, PG, D); v_pool: bf16
+    [num_pages, Hkv, PG/B, D, B] with B = min(PG, 32) (see include/hswa.h);
+    block_table: int32 [ns, stride].
     """
 
     def __init__(self, k_pool, v_pool, block_table):
-        if k_pool.dim() != 4 or v_pool.dim() != 5 or block_table.dim() != 2:
-            raise ValueError("k_pool is 4-D, v_pool 5-D, the block table 2-D")
-        npg, hkv, pg, d = k_pool.shape
+        if k_pool.dim() != 8 or v_pool.dim() != 5 or block_table.dim() != 2:
+            raise ValueError("k_pool is 8-D, v_pool 5-D, the block table 2-D")
+        npg, hkv, d, vb = v_pool.shape[0], v_pool.shape[1], v_pool.shape[3], v_pool.shape[4]
+        pg = v_pool.shape[2] * vb
         if tuple(v_pool.shape) != v_pool_shape(npg, hkv, pg, d):
-            raise ValueError("v_pool must be [num_pages, Hkv, PG/VB, D, VB] with VB = min(PG, 32)")
+            raise ValueError("v_pool must be [num_pages, Hkv, PG/B, D, B] with B = min(PG, 32)")
+        if tuple(k_pool.shape) != k_pool_shape(npg, hkv, pg, d):
+            raise ValueError("k_pool must be k_pool_shape(num_pages, Hkv, PG, D)")
         self.k_pool, self.v_pool, self.block_table = k_pool, v_pool, block_table
         self.num_pages, self.stride = int(npg), int(block_table.shape[1])
 

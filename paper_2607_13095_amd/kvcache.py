@@ -39,7 +39,8 @@ class LayerKV:
                       else max(1, max(-(-int(n) // pg) for n in final_lens)))
         self.table_host = hswa.build_block_table(layer, pg, final_lens, perm, stride)
         self.block_table = torch.from_numpy(self.table_host).to(device)
-        self.k_pool = torch.full((self.num_pages, hkv, pg, d), fill, dtype=torch.bfloat16, device=device)
+        self.k_pool = torch.full(hswa.k_pool_shape(self.num_pages, hkv, pg, d), fill, dtype=torch.bfloat16,
+                                 device=device)
         self.v_pool = torch.full(hswa.v_pool_shape(self.num_pages, hkv, pg, d), fill, dtype=torch.bfloat16,
                                  device=device)
         self.cache = hswa.Cache(self.k_pool, self.v_pool, self.block_table)

@@ -22,7 +22,7 @@ D = 128
 
 
 def _pools(num_pages, hkv, pg):
-    k = torch.full((num_pages, hkv, pg, D), float("nan"), dtype=torch.bfloat16, device="cuda")
+    k = torch.full(hswa.k_pool_shape(num_pages, hkv, pg, D), float("nan"), dtype=torch.bfloat16, device="cuda")
     v = torch.full(hswa.v_pool_shape(num_pages, hkv, pg, D), float("nan"), dtype=torch.bfloat16, device="cuda")
     return k, v
 

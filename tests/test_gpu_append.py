@@ -62,7 +62,7 @@ def test_append_bit_exact(gpu_lib, case):
         for b in range(ns):
             for (entry, off), pos in OL.ring_positions(window, pg, final[b]).items():
                 page = kv.table_host[b][entry]
-                assert np.array_equal(to_bits(kv.k_pool[page, :, off, :]), hist.k[b][pos])
+                assert np.array_equal(OL.k_rows(to_bits(kv.k_pool), page, off), hist.k[b][pos])
         assert r == hswa.ring_pages(window, pg)
 
 

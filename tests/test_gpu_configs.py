@@ -81,7 +81,7 @@ def test_cfg_swa_prefill_512(gpu_lib):
     vp = to_bits(kv.v_pool)
     for t in np.nonzero(want >= 0)[0]:
         s = int(want[t])
-        assert np.array_equal(kp[s // pg, :, s % pg, :], k[t])
+        assert np.array_equal(OL.k_rows(kp, s // pg, s % pg), k[t])
         vb = hswa.v_block(pg)
         assert np.array_equal(vp[s // pg, :, (s % pg) // vb, :, (s % pg) % vb], v[t])
 

@@ -72,7 +72,7 @@ def test_poisoned_stale_ring_slots(gpu_lib):
         for (entry, off), pos in OL.ring_positions(window, pg, L).items():
             if pos < L - window:  # held by the ring but outside the window of the query at L-1
                 page = int(kv.table_host[b][entry])
-                kv.k_pool[page, :, off, :] = float("nan")
+                kv.k_pool[OL.k_slot(kv.k_pool.shape, page, off)] = float("nan")
                 vb = hswa.v_block(pg)
                 kv.v_pool[page, :, off // vb, :, off % vb] = float("nan")
                 poisoned += 1

@@ -59,23 +59,74 @@ def test_slot_mapping_full_hand_worked():
 
 
 def test_apply_append_hand_worked():
-    pg, hkv, d = 2, 1, 3
-    kp = np.zeros((2, hkv, pg, d), dtype=np.uint16)
-    vp = np.zeros((2, hkv, 1, d, pg), dtype=np.uint16)  # one block of VB = PG = 2 keys
-    kn = np.array([[[1, 2, 3]], [[4, 5, 6]], [[7, 8, 9]]], dtype=np.uint16)
-    vn = kn + 100
-    k2, v2 = Lo.apply_append(kp, vp, [3, -1, 0], kn, vn)
-    # slot 3 = page 1, offset 1; slot 0 = page 0, offset 0; token 1 dropped
-    assert k2[1, 0, 1].tolist() == [1, 2, 3] and k2[0, 0, 0].tolist() == [7, 8, 9]
-    assert v2[1, 0, 0, :, 1].tolist() == [101, 102, 103] and v2[0, 0, 0, :, 0].tolist() == [107, 108, 109]
-    assert int(k2.sum()) == 1 + 2 + 3 + 7 + 8 + 9
+    """PG = 16 (blocks of B = 16 keys), D = 32 (one slab). Slot 21 = page 1,
+    offset 5: bit 2 of 5 is set, so half 1, row 4 * (5 // 8) + 5 % 4 = 1;
+    slot 0 = page 0, half 0, row 0; token 1 (slot -1) is dropped."""
+    pg, hkv, d = 16, 1, 32
+    kp = np.zeros(Lo.k_pool_shape(2, hkv, pg, d), dtype=np.uint16)
+    assert kp.shape == (2, 1, 1, 2, 1, 4, 8, 8)
+    vp = np.zeros((2, hkv, 1, d, pg), dtype=np.uint16)
+    kn = np.arange(1, 1 + 3 * d, dtype=np.uint16).reshape(3, hkv, d)
+    vn = kn + 1000
+    k2, v2 = Lo.apply_append(kp, vp, [21, -1, 0], kn, vn)
+    assert k2[1, 0, 0, 1, 0, :, 1, :].reshape(d).tolist() == kn[0, 0].tolist()
+    assert k2[0, 0, 0, 0, 0, :, 0, :].reshape(d).tolist() == kn[2, 0].tolist()
+    assert int(k2.sum()) == int(kn[0].sum()) + int(kn[2].sum())
+    assert v2[1, 0, 0, :, 5].tolist() == vn[0, 0].tolist() and v2[0, 0, 0, :, 0].tolist() == vn[2, 0].tolist()
+    assert Lo.k_rows(k2, 1, 5).tolist() == kn[0].tolist()
+
+
+def test_k_layout_flat_offset_hand_worked():
+    """PG = 32, D = 64: in-page offset 13 (binary 1101: half 1, row 4*1 + 1 = 5),
+    dim 37 (slab 1, piece (37 // 8) % 4 = 0, element 5) sits at flat element
+    ((((1 * 2 + 1) * 4 + 0) * 16 + 5) * 8 + 5 = 1581 of the page-head."""
+    pg, hkv, d = 32, 1, 64
+    kp = np.zeros(Lo.k_pool_shape(1, hkv, pg, d), dtype=np.uint16)
+    kn = np.zeros((1, hkv, d), dtype=np.uint16)
+    kn[0, 0, 37] = 777
+    k2, _ = Lo.apply_append(kp, np.zeros((1, hkv, 1, d, 32), dtype=np.uint16), [13], kn, kn)
+    flat = k2.reshape(pg * d)
+    assert flat[1581] == 777 and int(flat.sum()) == 777
+
+
+def test_k_layout_mfma_operand_runs():
+    """PG = 64, D = 128: for 32-key block j, half h and slab t, the 16 keys
+    32 j + 8 (r // 4) + 4 h + r % 4 (r < 16) with dims 32 t + 8 q + e are one
+    contiguous 1 KiB run in the order of lane l = r + 16 q (16 bytes a lane)."""
+    pg, hkv, d = 64, 1, 128
+    kp = np.zeros(Lo.k_pool_shape(1, hkv, pg, d), dtype=np.uint16)
+    kn = np.arange(pg * d, dtype=np.uint16).reshape(pg, hkv, d)  # value = 128 * key + dim
+    k2, _ = Lo.apply_append(kp, np.zeros((1, hkv, 2, d, 32), dtype=np.uint16), list(range(pg)), kn, kn)
+    flat = k2.reshape(pg * d)
+    for j in range(2):
+        for h in range(2):
+            for t in range(4):
+                run = flat[j * 4096 + h * 2048 + t * 512: j * 4096 + h * 2048 + (t + 1) * 512].reshape(64, 8)
+                for lane in range(64):
+                    r, q = lane % 16, lane // 16
+                    key = 32 * j + 8 * (r // 4) + 4 * h + r % 4
+                    assert run[lane].tolist() == [128 * key + 32 * t + 8 * q + e for e in range(8)]
+
+
+@pytest.mark.parametrize("pg", [16, 32, 64, 256])
+def test_k_layout_is_a_bijection(pg):
+    """Every (key, dim) of a page-head lands on its own element: writing all
+    keys with distinct values fills the page exactly once."""
+    d = 128
+    kp = np.zeros(Lo.k_pool_shape(1, 1, pg, d), dtype=np.int64)
+    vals = np.arange(1, 1 + pg * d, dtype=np.int64).reshape(pg, 1, d)
+    vb = min(pg, 32)
+    k2, _ = Lo.apply_append(kp, np.zeros((1, 1, pg // vb, d, vb), dtype=np.int64), list(range(pg)), vals, vals)
+    assert sorted(k2.reshape(-1).tolist()) == list(range(1, 1 + pg * d))
+    for o in (0, pg // 2 + 5, pg - 1):
+        assert Lo.k_rows(k2, 0, o).tolist() == vals[o].tolist()
 
 
 def test_apply_append_v_blocks_hand_worked():
     """PG = 64: V is stored in two blocks of 32 keys; in-page offset 40 is key 8
     of block 1, so its dims sit at flat element 1*32*D + d*32 + 8 of the page."""
-    pg, hkv, d = 64, 2, 4
-    kp = np.zeros((3, hkv, pg, d), dtype=np.uint16)
+    pg, hkv, d = 64, 2, 32
+    kp = np.zeros(Lo.k_pool_shape(3, hkv, pg, d), dtype=np.uint16)
     vp = np.zeros((3, hkv, 2, d, 32), dtype=np.uint16)
     kn = np.arange(1, 1 + hkv * d, dtype=np.uint16).reshape(1, hkv, d)
     _, v2 = Lo.apply_append(kp, vp, [2 * 64 + 40], kn, kn + 50)
@@ -86,6 +137,8 @@ def test_apply_append_v_blocks_hand_worked():
     assert int((v2 != 0).sum()) == hkv * d
     with pytest.raises(ValueError):
         Lo.apply_append(kp, np.zeros((3, hkv, d, pg), dtype=np.uint16)[..., None], [0], kn, kn)
+    with pytest.raises(ValueError):
+        Lo.apply_append(np.zeros((3, hkv, pg, d), dtype=np.uint16), vp, [0], kn, kn)
 
 
 @pytest.mark.parametrize("window,pg", [(4, 2), (128, 16), (128, 64), (1, 16), (129, 64), (5, 4)])
