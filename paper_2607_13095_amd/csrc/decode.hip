@@ -385,16 +385,19 @@ __global__ __launch_bounds__(kWave * kWaves<kSplit>) __attribute__((amdgpu_waves
 
 // Log-sum-exp merge of the split partials: one wave per (sequence, query head).
 // Lane j reads the log-sum-exp of pieces j, j+64, ...; the weights are then
-// broadcast piece by piece while every lane accumulates two output dims.
+// broadcast by readlane while the two half-waves accumulate even and odd
+// pieces, four output dims a lane (16-byte loads, 16 pieces in flight a step).
 __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(DecodeParams p) {
   const int lane = threadIdx.x & (kWave - 1);
   const int64_t idx = (int64_t)blockIdx.x * (kMergeThreads / kWave) + (threadIdx.x / kWave);
   if (idx >= (int64_t)p.ns * p.nq * p.hq) return;
   const int b = (int)(idx / ((int64_t)p.nq * p.hq));
   const int ctx = min(p.ctx_lens[b], p.max_ctx);
-  uint32_t *dst = reinterpret_cast<uint32_t *>(p.out + idx * kHeadDim) + lane;
+  const int half = lane >> 5, d4 = (lane & 31) * 4;
+  u32x2 *dst = reinterpret_cast<u32x2 *>(p.out + idx * kHeadDim + d4);
+  const u32x2 zero = {0u, 0u};
   if (ctx < 1) {
-    *dst = 0u;
+    if (half == 0) *dst = zero;
     return;
   }
   const int nsplit = (ctx - 1) / p.split_len + 1;
@@ -405,34 +408,47 @@ __global__ __launch_bounds__(kMergeThreads) void decode_merge_kernel(DecodeParam
   for (int off = 8; off >= 1; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off, kWave));
   mx = max_xor32(max_xor16(mx));
   if (mx == -INFINITY) {  // a query that sees no key (multi-query rows before position 0)
-    *dst = 0u;
+    if (half == 0) *dst = zero;
     return;
   }
-  const float *po = p.ws_o + idx * p.max_splits * kHeadDim + 2 * lane;
-  float wsum = 0.f, o0 = 0.f, o1 = 0.f;
+  const float *po = p.ws_o + idx * p.max_splits * kHeadDim + d4;
+  float wsum = 0.f;
+  f32x4 o = {0.f, 0.f, 0.f, 0.f};
   for (int s0 = 0; s0 < nsplit; s0 += kWave) {
     const int s = s0 + lane;
     const float w = s < nsplit ? fast_exp2(lse[s] - mx) : 0.f;
     const int n = min(kWave, nsplit - s0);
-    // 8 pieces per step: their loads are independent and go out together
-    for (int k0 = 0; k0 < n; k0 += 8) {
-      float2 v[8];
-#pragma unroll
-      for (int k = 0; k < 8; ++k)
-        v[k] = k0 + k < n ? *reinterpret_cast<const float2 *>(po + (int64_t)(s0 + k0 + k) * kHeadDim)
-                          : float2{0.f, 0.f};
+    for (int k0 = 0; k0 < n; k0 += 16) {
+      f32x4 v[8];
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
-        const float wk = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, w), min(k0 + k, kWave - 1)));
-        const float wkk = k0 + k < n ? wk : 0.f;
-        wsum += wkk;
-        o0 = fmaf(wkk, v[k].x, o0);
-        o1 = fmaf(wkk, v[k].y, o1);
+        const int pc = k0 + 2 * k + half;
+        const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+        v[k] = pc < n ? *reinterpret_cast<const f32x4 *>(po + (int64_t)(s0 + pc) * kHeadDim) : z;
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int pe = min(k0 + 2 * k, kWave - 1), pd = min(k0 + 2 * k + 1, kWave - 1);
+        const float we = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, w), pe));
+        const float wd = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, w), pd));
+        const int pc = k0 + 2 * k + half;
+        const float wk = pc < n ? (half ? wd : we) : 0.f;
+        wsum += wk;
+        o += wk * v[k];
       }
     }
   }
+  // the two halves hold even and odd pieces: add across lanes l and l ^ 32
+  wsum = sum_xor32(wsum);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) o[i] = sum_xor32(o[i]);
   const float inv = 1.f / wsum;
-  *dst = pack_bf16x2(o0 * inv, o1 * inv);
+  if (half == 0) {
+    u32x2 w2;
+    w2[0] = pack_bf16x2(o[0] * inv, o[1] * inv);
+    w2[1] = pack_bf16x2(o[2] * inv, o[3] * inv);
+    *dst = w2;
+  }
 }
 
 }  // namespace

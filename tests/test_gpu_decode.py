@@ -70,14 +70,16 @@ def test_decode_window_one_is_exact_value(gpu_lib):
 @pytest.mark.parametrize("pg", [16, 64])
 def test_decode_full_split_boundaries(gpu_lib, pg):
     shape = hswa.Shape(64, 8, 128, pg)
-    ns = 10
+    ns = 12
     maxc = 5000
     sl = hswa.decode_split_len(shape, ns, maxc)
     assert sl % 256 == 0 and sl > 0
     tl = sl // 4
-    # contexts (keys incl. the new token, c + 1) at piece boundaries +-1, at
-    # quarter pieces, shorter than one piece, and the max
-    ctxs = [sl - 2, sl - 1, sl, 2 * sl - 1, 2 * sl, sl + tl - 1, sl + tl, 2 * sl + 3 * tl, tl - 1, maxc - 1]
+    # contexts (keys incl. the new token, c + 1) at piece boundaries +-1 (the
+    # last piece then holds only the newest key), at quarter pieces, just
+    # below three pieces, shorter than one piece, and the max
+    ctxs = [sl - 2, sl - 1, sl, 2 * sl - 1, 2 * sl, sl + tl - 1, sl + tl, 2 * sl + 3 * tl, tl - 1, 3 * sl - 2,
+            3 * sl - 1, maxc - 1]
     assert len(ctxs) == ns and max(c + 1 for c in ctxs) == maxc and maxc > sl
     print(f"[decode-full-split] pg={pg} split_len={sl}", flush=True)
     gpu, ref = run_decode("full", 0, pg, 64, 8, ctxs, (203, pg))

@@ -65,14 +65,27 @@ def test_decode_multi_groups(gpu_lib, hq, hkv):
 
 
 def test_decode_multi_split_tail(gpu_lib):
-    """FULL pieces: contexts (c + nq) one past a piece boundary, so the last
-    piece holds only the newest key, which the first three queries do not see."""
-    nq, ns, maxc = 4, 6, 6000
+    """FULL pieces: final contexts (c + nq) one past a piece boundary, so the
+    last piece holds only the newest key, which the first three queries do not
+    see; then quarter-piece offsets, an exact boundary, one below three pieces
+    and the max."""
+    nq, ns, maxc = 4, 7, 6000
     shape = hswa.Shape(64, 8, D, 64)
     sl = hswa.decode_split_len(shape, ns, maxc)
-    ctxs = [sl + 1 - nq, 2 * sl + 1 - nq, 2 * sl + 2 - nq, sl - nq, 3 * sl + 3 - nq, maxc - nq]
+    tl = sl // 4
+    finals = [sl + 1, 2 * sl + 1, 3 * sl + 2 * tl + 1, 2 * sl + 3 * tl + 2, sl, 3 * sl - 1, maxc]
+    ctxs = [f - nq for f in finals]
     gpu, ref, _ = run_multi("full", 0, 64, 64, 8, ctxs, nq, (902,))
     assert_close(gpu, ref, f"decode multi split tail, split_len {sl}")
+
+
+def test_decode_multi_split_no_visible_key(gpu_lib):
+    """Split path (max context above one piece) with a sequence whose context
+    is below num_queries: its first queries see no key and get zero rows from
+    the merge (every partial has log-sum-exp -inf)."""
+    gpu, ref, _ = run_multi("full", 0, 64, 64, 8, [0, 6000], 4, (905,), ctx_override=[2, 6004])
+    assert np.all(gpu[0][:2] == 0) and np.all(gpu[0][2:] != 0)
+    assert_close(gpu, ref, "decode multi split, no visible key")
 
 
 def test_decode_multi_one_equals_decode(gpu_lib):
