@@ -19,8 +19,10 @@ namespace {
 
 constexpr int kTokPerBlock = 8;
 constexpr int kThreads = 256;
+constexpr int kLdsSeqs = 4096;  // batches up to this size search cu_seqlens in LDS
 
 // Sequence of flattened token t: the b with cu[b] <= t < cu[b+1] (-1 if none).
+// `cu` is the LDS copy of cu_seqlens when it fits, else the global array.
 __device__ int find_seq(const int32_t *cu, int ns, int t) {
   int lo = 0, hi = ns;  // answer in [0, ns)
   if (ns <= 0 || t < cu[0] || t >= cu[ns]) return -1;
@@ -31,12 +33,12 @@ __device__ int find_seq(const int32_t *cu, int ns, int t) {
   return lo;
 }
 
-__device__ int64_t slot_of_token(const AppendParams &p, int t) {
-  const int b = find_seq(p.cu_seqlens, p.ns, t);
+__device__ int64_t slot_of_token(const AppendParams &p, const int32_t *cu, int t) {
+  const int b = find_seq(cu, p.ns, t);
   if (b < 0) return -1;
   const int64_t start = p.start_pos[b];
-  const int64_t j = start + (t - p.cu_seqlens[b]);
-  const int64_t len_after = start + (p.cu_seqlens[b + 1] - p.cu_seqlens[b]);
+  const int64_t j = start + (t - cu[b]);
+  const int64_t len_after = start + (cu[b + 1] - cu[b]);
   if (j < 0) return -1;
   const PoolView &pv = p.pool;
   const int64_t pg = int64_t(1) << pv.pg_shift;
@@ -55,12 +57,20 @@ __device__ int64_t slot_of_token(const AppendParams &p, int t) {
 // KV head: 8 K rows of 256 bytes and 8 x 128 V values.
 __global__ __launch_bounds__(kThreads) void kv_append_kernel(AppendParams p) {
   __shared__ int64_t s_slot[kTokPerBlock];
+  __shared__ int32_t s_cu[kLdsSeqs + 1];
   const int t0 = blockIdx.x * kTokPerBlock;
   const int g = blockIdx.y;
   const int tid = threadIdx.x;
   const int ntok = min(kTokPerBlock, p.total_tokens - t0);
+  // One coalesced load of cu_seqlens instead of a chain of dependent loads in
+  // the binary search.
+  const bool lds_cu = p.ns <= kLdsSeqs;
+  if (lds_cu) {
+    for (int i = tid; i <= p.ns; i += kThreads) s_cu[i] = p.cu_seqlens[i];
+  }
+  __syncthreads();
   if (tid < ntok) {
-    const int64_t s = slot_of_token(p, t0 + tid);
+    const int64_t s = slot_of_token(p, lds_cu ? s_cu : p.cu_seqlens, t0 + tid);
     s_slot[tid] = s;
     if (p.slot_out && g == 0) p.slot_out[t0 + tid] = s;
   }
