@@ -46,11 +46,11 @@ MFMA_BF16_PEAK_TFLOPS = 2516.6
 # once they change the benchmark reports null until it is measured again.
 MEASURED_TRAFFIC = {
     "decode_full": {"sources": ["decode.hip", "hswa_common.h", "hswa_launch.h"],
-                    "sha256": "087fae7adfe6543279d19194bb2934fa52a3f34e9e0844e22133539a4ec6c223",
-                    "fetch_bytes": 4134086042, "write_bytes": 66944614},
+                    "sha256": "3f0627ec68b9ebc5c056137cba415beab5bea967ad1fc4f946905a1391818d35",
+                    "fetch_bytes": 4136497562, "write_bytes": 67865907},
     "prefill_full": {"sources": ["prefill.hip", "hswa_common.h", "hswa_launch.h"],
-                     "sha256": "2fadac2ca521139209ee458bdfce1828168cd33e2bedfeb2c51c72e9559e4da4",
-                     "fetch_bytes": 1491017664, "write_bytes": 134217728},
+                     "sha256": "91d1ed39ab605e134f4627b0b54f80812d2ae3891a40369480b9d53066deb479",
+                     "fetch_bytes": 1340659661, "write_bytes": 134217728},
 }
 
 
@@ -83,6 +83,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prefill", action="store_true")
+    ap.add_argument("--roofline-only", action="store_true",
+                    help="only the decode step and the prefill calls the roofline entries time (for counter runs)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target oracle time for the CPU baseline")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 1 GiB device copy three times (reference for HBM byte counters)")
@@ -165,22 +167,34 @@ class DecodeBench:
             self.bytes[L["kind"]] = keys * row + qo
         self.append_bytes = len(self.layers) * ns * nq * hkv * d * 2 * 2 * 2   # read + write
 
-    def step(self, full_events=None):
+    def step(self):
         from paper_2607_13095_amd import hswa
 
         for L in self.layers:
             hswa.kv_append(L["layer"], self.shape, L["kv"].cache, L["k_new"], L["v_new"], self.cu1, self.start)
-            if L["kind"] == "full" and full_events is not None:
-                full_events[0].record()
             self.decode(L)
-            if L["kind"] == "full" and full_events is not None:
-                full_events[1].record()
 
     def decode(self, L):
         from paper_2607_13095_amd import hswa
 
         fn = hswa.decode if self.nq == 1 else hswa.decode_multi
         fn(L["layer"], self.shape, L["kv"].cache, L["q"], self.ctx_lens, self.maxc, L["out"], workspace=L["ws"])
+
+    def time_kind_back_to_back(self, kind, reps):
+        """Mean time of one layer kind's decode call over reps calls issued back
+        to back between one pair of HIP events on the current stream."""
+        import torch
+
+        L = next(x for x in self.layers if x["kind"] == kind)
+        self.decode(L)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record()
+        for _ in range(reps):
+            self.decode(L)
+        b.record()
+        b.synchronize()
+        return a.elapsed_time(b) / reps
 
     def time_kind(self, kind, reps=20):
         """Event timing of one layer kind's decode call alone (median of reps)."""
@@ -503,6 +517,35 @@ def prefix_tree_report(window=128, convs=128, turns=8, turn_len=512, seed=11):
             "host_us_per_release": round(t_rel / n_ins * 1e6, 1)}
 
 
+def extra_reports(wl, full_avg):
+    """Multi-query decode, window-safe prefix tree and explicit-release allocator reports."""
+    import torch
+
+    log("[bench] multi-query decode (1 + 3 queries per sequence)")
+    mt = DecodeBench(wl, nq=4)
+    for _ in range(3):
+        mt.step()
+    torch.cuda.synchronize()
+    mt_full = mt.time_kind("full")
+    mt_swa = mt.time_kind("swa")
+    mtp = {"queries_per_seq": 4, "full_ms": round(mt_full, 5), "swa_ms": round(mt_swa, 5),
+           "full_gbs": round(mt.bytes["full"] / (mt_full * 1e-3) / 1e9, 1),
+           "full_ms_vs_one_query": round(mt_full / full_avg, 3)}
+    log(f"[bench] multi-query decode: {mtp}")
+    del mt
+    torch.cuda.empty_cache()
+
+    log("[bench] window-safe prefix tree")
+    prefix_rep = prefix_tree_report()
+    log(f"[bench] prefix tree: {prefix_rep}")
+
+    log("[bench] explicit-release allocator")
+    alloc_rep = allocator_report(wl)
+    log(f"[bench] allocator: {alloc_rep}")
+
+    return mtp, prefix_rep, alloc_rep
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -525,21 +568,20 @@ def main():
     for _ in range(args.warmup):
         db.step()
     torch.cuda.synchronize()
-    full_ms = []
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    per = [[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     start.record()
-    for k in range(args.steps):
-        db.step(full_events=per[k])
+    for _ in range(args.steps):
+        db.step()
     stop.record()
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(stop)
-    full_ms = [a.elapsed_time(b) for a, b in per]
     ms_step = total_ms / args.steps
     dec_bytes = sum(db.bytes.values())
     value = dec_bytes / (ms_step * 1e-3) / 1e9
-    full_avg = float(np.mean(full_ms))
+    # The roofline kernel alone: FULL-layer decode calls back to back on the
+    # stream they run on, one HIP event pair around them (no host gap per call).
+    full_avg = db.time_kind_back_to_back("full", max(args.steps, 10))
     full_gbs = db.bytes["full"] / (full_avg * 1e-3) / 1e9
     swa_ms = db.time_kind("swa")
     log(f"[bench] decode step {ms_step:.4f} ms; FULL decode {full_avg:.4f} ms ({full_gbs:.0f} GB/s); "
@@ -565,38 +607,23 @@ def main():
                          "algorithmic_flops": pb.flops["full"]},
         }
         log(f"[bench] prefill FULL {f_ms:.3f} ms = {f_tf:.1f} TFLOP/s; SWA {s_ms:.3f} ms = {s_gbs:.0f} GB/s")
-        log("[bench] layerwise prefetch (70-layer prefill stack, prefix from pinned host memory)")
-        prefill["prefetch"] = prefetch_report(pb)
-        log(f"[bench] prefetch: {prefill['prefetch']}")
+        if not args.roofline_only:
+            log("[bench] layerwise prefetch (70-layer prefill stack, prefix from pinned host memory)")
+            prefill["prefetch"] = prefetch_report(pb)
+            log(f"[bench] prefetch: {prefill['prefetch']}")
         del pb
         torch.cuda.empty_cache()
 
-    log("[bench] multi-query decode (1 + 3 queries per sequence)")
-    mt = DecodeBench(wl, nq=4)
-    for _ in range(3):
-        mt.step()
-    torch.cuda.synchronize()
-    mt_full = mt.time_kind("full")
-    mt_swa = mt.time_kind("swa")
-    mtp = {"queries_per_seq": 4, "full_ms": round(mt_full, 5), "swa_ms": round(mt_swa, 5),
-           "full_gbs": round(mt.bytes["full"] / (mt_full * 1e-3) / 1e9, 1),
-           "full_ms_vs_one_query": round(mt_full / full_avg, 3)}
-    log(f"[bench] multi-query decode: {mtp}")
-    del mt
-    torch.cuda.empty_cache()
+    mtp = prefix_rep = alloc_rep = cpu = None
+    if args.roofline_only:
+        args.no_cpu_baseline = True
+    else:
+        mtp, prefix_rep, alloc_rep = extra_reports(wl, full_avg)
 
-    log("[bench] window-safe prefix tree")
-    prefix_rep = prefix_tree_report()
-    log(f"[bench] prefix tree: {prefix_rep}")
-
-    log("[bench] explicit-release allocator")
-    alloc_rep = allocator_report(wl)
-    log(f"[bench] allocator: {alloc_rep}")
-
-    cpu = None
     if not args.no_cpu_baseline:
         log("[bench] CPU baseline (oracle)")
         cpu = db.cpu_baseline(args.cpu_seconds)
+
 
     line = {
         "metric": "decode attn HBM GB/s (% peak) + prefill attn TFLOP/s (% MFMA), W=128",
