@@ -517,6 +517,229 @@ def prefix_tree_report(window=128, convs=128, turns=8, turn_len=512, seed=11):
             "host_us_per_release": round(t_rel / n_ins * 1e6, 1)}
 
 
+def stack70_report(steps=5, warmup=2):
+    """The 70-layer hybrid decode step (10 FULL + 60 SWA layers, 16 sequences at
+    a 131072-token context): every layer's pools hold its own synthetic KV
+    (86 GB of FULL pages, 12 MiB per SWA layer), and one step appends the new
+    token and decodes it in every layer. Timed eagerly and as a replayed graph
+    of the step, plus per-kind parts; also reports the pool bytes per kind."""
+    import torch
+
+    import synth
+    from paper_2607_13095_amd import hswa
+    from paper_2607_13095_amd.kvcache import LayerKV, pages_for
+
+    wl = synth.stack70_decode()
+    dev = "cuda"
+    hq, hkv, d, pg, W = wl.hq, wl.hkv, wl.head_dim, wl.page_size, wl.window
+    ns = wl.ns
+    ctx = np.asarray(wl.prefix, dtype=np.int64)
+    final = (ctx + 1).tolist()
+    maxc = int(max(final))
+    shape = hswa.Shape(hq, hkv, d, pg)
+    i32 = lambda x: torch.as_tensor(np.asarray(x, dtype=np.int32), device=dev)  # noqa: E731
+    ring = hswa.ring_pages(W, pg)
+    ws = torch.empty(max(1, hswa.decode_workspace_bytes(shape, ns, maxc)), dtype=torch.uint8, device=dev)
+    layers = []
+    for li, kind in enumerate(wl.layers):
+        layer = hswa.Layer.swa(W) if kind == "swa" else hswa.Layer.full()
+        kv = LayerKV(layer, shape, final, perm=synth.page_permutation(pages_for(layer, pg, final), wl.seed, li))
+        # cached history: every position for FULL (four sequences at a time),
+        # the positions the ring keeps for SWA
+        first = np.zeros(ns, dtype=np.int64) if kind == "full" else np.maximum(0, ctx - ring * pg)
+        for b0 in range(0, ns, 4):
+            sl = slice(b0, min(ns, b0 + 4))
+            lens = ctx[sl] - first[sl]
+            T = int(lens.sum())
+            kh = synth.torch_normal_bf16((T, hkv, d), dev, wl.seed, li, b0, synth.TAG_K)
+            vh = synth.torch_normal_bf16((T, hkv, d), dev, wl.seed, li, b0, synth.TAG_V)
+            sub = hswa.Cache(kv.k_pool, kv.v_pool, kv.block_table[sl])
+            hswa.kv_append(layer, shape, sub, kh, vh, i32(synth.cu_seqlens(lens)), i32(first[sl]))
+            del kh, vh
+        layers.append(dict(kind=kind, layer=layer, kv=kv,
+                           k_new=synth.torch_normal_bf16((ns, hkv, d), dev, wl.seed, li, 0, synth.TAG_KDEC),
+                           v_new=synth.torch_normal_bf16((ns, hkv, d), dev, wl.seed, li, 0, synth.TAG_VDEC),
+                           q=synth.torch_normal_bf16((ns, hq, d), dev, wl.seed, li, 0, synth.TAG_QDEC),
+                           out=torch.empty((ns, hq, d), dtype=torch.bfloat16, device=dev)))
+    torch.cuda.synchronize()
+    cu1, start, lens_dev = i32(np.arange(ns + 1)), i32(ctx), i32(final)
+
+    def run(kinds):
+        for L in layers:
+            if L["kind"] in kinds:
+                hswa.kv_append(L["layer"], shape, L["kv"].cache, L["k_new"], L["v_new"], cu1, start)
+                hswa.decode(L["layer"], shape, L["kv"].cache, L["q"], lens_dev, maxc, L["out"], workspace=ws)
+
+    def timed(fn, n):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(n):
+            fn()
+        b.record()
+        b.synchronize()
+        return a.elapsed_time(b) / n
+
+    step_ms = timed(lambda: run(("full", "swa")), steps)
+    full_ms = timed(lambda: run(("full",)), steps)
+    swa_ms = timed(lambda: run(("swa",)), steps)
+    graph_ms = None
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        run(("full", "swa"))
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        run(("full", "swa"))
+    graph_ms = timed(g.replay, steps)
+    row, qo = hkv * d * 2 * 2, 2 * ns * hq * d * 2
+    nfull = sum(1 for L in layers if L["kind"] == "full")
+    nswa = len(layers) - nfull
+    full_bytes = nfull * (int(np.sum(ctx + 1)) * row + qo)
+    swa_bytes = nswa * (int(np.sum(np.minimum(W, ctx + 1))) * row + qo)
+    page_b = hswa.page_bytes(shape)
+    rep = {
+        "workload": wl.name, "layers": len(layers), "full_layers": nfull, "swa_layers": nswa,
+        "step_ms": round(step_ms, 4), "graph_step_ms": round(graph_ms, 4),
+        "step_gbs": round((full_bytes + swa_bytes) / (step_ms * 1e-3) / 1e9, 1),
+        "graph_step_gbs": round((full_bytes + swa_bytes) / (graph_ms * 1e-3) / 1e9, 1),
+        "frac_hbm": round((full_bytes + swa_bytes) / (min(step_ms, graph_ms) * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "full_layers_ms": round(full_ms, 4), "full_gbs": round(full_bytes / (full_ms * 1e-3) / 1e9, 1),
+        "swa_layers_ms": round(swa_ms, 4), "swa_gbs": round(swa_bytes / (swa_ms * 1e-3) / 1e9, 1),
+        "algorithmic_bytes": full_bytes + swa_bytes,
+        "pool_bytes_per_full_layer": 2 * pages_for(hswa.Layer.full(), pg, final) * page_b,
+        "pool_bytes_per_swa_layer": 2 * pages_for(hswa.Layer.swa(W), pg, final) * page_b,
+    }
+    del layers, ws, g
+    torch.cuda.empty_cache()
+    return rep
+
+
+def mixed_report(reps=10, warmup=3):
+    """Mixed prefill + decode step of one SWA and one FULL layer: 8 chunks of
+    4096 tokens over cached prefixes uniform in [0, 65536], plus 256 decodes with
+    log-normal contexts. Per layer the step runs the chunks' prefill and append,
+    then the decodes' append and decode. Reports each call's rate and the step
+    time against the sum of the calls' rooflines."""
+    import torch
+
+    import synth
+    from paper_2607_13095_amd import hswa
+    from paper_2607_13095_amd.kvcache import LayerKV, pages_for
+
+    wl = synth.mixed_step()
+    dev = "cuda"
+    hq, hkv, d, pg, W = wl.hq, wl.hkv, wl.head_dim, wl.page_size, wl.window
+    pre = np.asarray(wl.prefix, dtype=np.int64)
+    new = np.asarray(wl.new, dtype=np.int64)
+    is_dec = np.asarray(wl.decode_mask, dtype=bool)
+    npf = int((~is_dec).sum())
+    final = (pre + new).tolist()
+    shape = hswa.Shape(hq, hkv, d, pg)
+    i32 = lambda x: torch.as_tensor(np.asarray(x, dtype=np.int32), device=dev)  # noqa: E731
+    ring = hswa.ring_pages(W, pg)
+    Tp = int(new[:npf].sum())
+    ndec = int(is_dec.sum())
+    dec_lens = (pre[npf:] + 1)
+    maxd = int(dec_lens.max())
+    ws = torch.empty(max(1, hswa.decode_workspace_bytes(shape, ndec, maxd)), dtype=torch.uint8, device=dev)
+    layers = []
+    for li, kind in enumerate(wl.layers):
+        layer = hswa.Layer.swa(W) if kind == "swa" else hswa.Layer.full()
+        kv = LayerKV(layer, shape, final, perm=synth.page_permutation(pages_for(layer, pg, final), wl.seed, li))
+        first = np.zeros(len(pre), dtype=np.int64) if kind == "full" else np.maximum(0, pre - ring * pg)
+        for b0 in range(0, len(pre), 32):
+            sl = slice(b0, min(len(pre), b0 + 32))
+            lens = pre[sl] - first[sl]
+            T = int(lens.sum())
+            if T == 0:
+                continue
+            kh = synth.torch_normal_bf16((T, hkv, d), dev, wl.seed, li, b0, synth.TAG_K)
+            vh = synth.torch_normal_bf16((T, hkv, d), dev, wl.seed, li, b0, synth.TAG_V)
+            sub = hswa.Cache(kv.k_pool, kv.v_pool, kv.block_table[sl])
+            hswa.kv_append(layer, shape, sub, kh, vh, i32(synth.cu_seqlens(lens)), i32(first[sl]))
+            del kh, vh
+        layers.append(dict(
+            kind=kind, layer=layer, kv=kv,
+            cp=hswa.Cache(kv.k_pool, kv.v_pool, kv.block_table[:npf]),
+            cd=hswa.Cache(kv.k_pool, kv.v_pool, kv.block_table[npf:]),
+            qp=synth.torch_normal_bf16((Tp, hq, d), dev, wl.seed, li, 1, synth.TAG_Q),
+            kp=synth.torch_normal_bf16((Tp, hkv, d), dev, wl.seed, li, 1, synth.TAG_K),
+            vp=synth.torch_normal_bf16((Tp, hkv, d), dev, wl.seed, li, 1, synth.TAG_V),
+            op=torch.empty((Tp, hq, d), dtype=torch.bfloat16, device=dev),
+            qd=synth.torch_normal_bf16((ndec, hq, d), dev, wl.seed, li, 2, synth.TAG_QDEC),
+            kd=synth.torch_normal_bf16((ndec, hkv, d), dev, wl.seed, li, 2, synth.TAG_KDEC),
+            vd=synth.torch_normal_bf16((ndec, hkv, d), dev, wl.seed, li, 2, synth.TAG_VDEC),
+            od=torch.empty((ndec, hq, d), dtype=torch.bfloat16, device=dev)))
+    torch.cuda.synchronize()
+    cup, prep = i32(synth.cu_seqlens(new[:npf])), i32(pre[:npf])
+    cud, startd, lensd = i32(np.arange(ndec + 1)), i32(pre[npf:]), i32(dec_lens)
+    maxchunk = int(new[:npf].max())
+
+    def prefill(L):
+        hswa.prefill(L["layer"], shape, L["cp"], L["qp"], L["kp"], L["vp"], cup, prep, maxchunk, L["op"])
+        hswa.kv_append(L["layer"], shape, L["cp"], L["kp"], L["vp"], cup, prep)
+
+    def decode(L):
+        hswa.kv_append(L["layer"], shape, L["cd"], L["kd"], L["vd"], cud, startd)
+        hswa.decode(L["layer"], shape, L["cd"], L["qd"], lensd, maxd, L["od"], workspace=ws)
+
+    def step():
+        for L in layers:
+            prefill(L)
+            decode(L)
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        b.synchronize()
+        return a.elapsed_time(b) / reps
+
+    by = {L["kind"]: L for L in layers}
+    t = {f"{what}_{k}": timed(lambda f=f, L=L: f(L)) for k, L in by.items()
+         for what, f in (("prefill", prefill), ("decode", decode))}
+    step_ms = timed(step)
+    row, hd = hkv * d * 2 * 2, 4 * d * hq
+    flops, pbytes, dbytes = {}, {}, {}
+    for k in by:
+        pairs = 0
+        for p_, c_ in zip(pre[:npf], new[:npf]):
+            pos = np.arange(p_, p_ + c_)
+            pairs += int((pos + 1).sum()) if k == "full" else int(np.minimum(W, pos + 1).sum())
+        flops[k] = hd * pairs
+        keys = int(np.sum(pre[:npf] + new[:npf])) if k == "full" else int(
+            sum(min(int(p_), W - 1) + int(c_) for p_, c_ in zip(pre[:npf], new[:npf])))
+        pbytes[k] = keys * row + 2 * Tp * hq * d * 2
+        dkeys = int(np.sum(dec_lens)) if k == "full" else int(np.sum(np.minimum(W, dec_lens)))
+        dbytes[k] = dkeys * row + 2 * ndec * hq * d * 2
+    roof = sum(max(flops[k] / (MFMA_BF16_PEAK_TFLOPS * 1e12), pbytes[k] / (HBM_PEAK_GBS * 1e9)) +
+               dbytes[k] / (HBM_PEAK_GBS * 1e9) for k in by) * 1e3
+    rep = {
+        "workload": wl.name, "step_ms": round(step_ms, 4), "roofline_sum_ms": round(roof, 4),
+        "frac_of_roofline": round(roof / step_ms, 4),
+        "prefill_full_ms": round(t["prefill_full"], 4),
+        "prefill_full_tflops": round(flops["full"] / (t["prefill_full"] * 1e-3) / 1e12, 1),
+        "prefill_swa_ms": round(t["prefill_swa"], 4),
+        "decode_full_ms": round(t["decode_full"], 4),
+        "decode_full_gbs": round(dbytes["full"] / (t["decode_full"] * 1e-3) / 1e9, 1),
+        "decode_swa_ms": round(t["decode_swa"], 4),
+        "note": "prefill and decode call times include their kv_append",
+    }
+    del layers, ws
+    torch.cuda.empty_cache()
+    return rep
+
+
 def extra_reports(wl, full_avg):
     """Multi-query decode, window-safe prefix tree and explicit-release allocator reports."""
     import torch
@@ -543,7 +766,15 @@ def extra_reports(wl, full_avg):
     alloc_rep = allocator_report(wl)
     log(f"[bench] allocator: {alloc_rep}")
 
-    return mtp, prefix_rep, alloc_rep
+    log("[bench] 70-layer hybrid decode step (16 x 131072 context)")
+    stack = stack70_report()
+    log(f"[bench] stack70: {stack}")
+
+    log("[bench] mixed prefill + decode step")
+    mixed = mixed_report()
+    log(f"[bench] mixed: {mixed}")
+
+    return mtp, prefix_rep, alloc_rep, stack, mixed
 
 
 def main():
@@ -614,11 +845,11 @@ def main():
         del pb
         torch.cuda.empty_cache()
 
-    mtp = prefix_rep = alloc_rep = cpu = None
+    mtp = prefix_rep = alloc_rep = stack = mixed = cpu = None
     if args.roofline_only:
         args.no_cpu_baseline = True
     else:
-        mtp, prefix_rep, alloc_rep = extra_reports(wl, full_avg)
+        mtp, prefix_rep, alloc_rep, stack, mixed = extra_reports(wl, full_avg)
 
     if not args.no_cpu_baseline:
         log("[bench] CPU baseline (oracle)")
@@ -651,6 +882,8 @@ def main():
         "multi_query_decode": mtp,
         "allocator": alloc_rep,
         "prefix_tree": prefix_rep,
+        "stack70_decode": stack,
+        "mixed_step": mixed,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

@@ -103,15 +103,19 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   const int G = p.group;
   const int npos = kRows / G;  // positions per workgroup
 
-  // XCD-aware order: workgroup ids that land on one XCD walk consecutive query
-  // tiles of the same (sequence, KV head) pair.
+  // XCD-aware order. Workgroup ids are dealt to the XCDs round-robin; the
+  // (sequence, KV head) pairs are dealt the same way, pair x + 8k to XCD x, so
+  // every query tile of a pair runs on one XCD and shares its K/V in that L2,
+  // while pairs of unequal length (different prefixes) spread over all XCDs.
+  // Within a pair the longest query tiles (the last ones) go first.
   const int ntq = (p.max_chunk_len + npos - 1) / npos;
-  const int64_t total = (int64_t)ntq * p.ns * p.hkv;
-  const int64_t per_xcd = (total + kXcds - 1) / kXcds;
-  const int64_t lin = (int64_t)(blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
-  if (lin >= total) return;
-  const int pair = (int)(lin / ntq);
-  const int tq = (int)(lin - (int64_t)pair * ntq);
+  const int npairs = p.ns * p.hkv;
+  const int xcd = (int)(blockIdx.x % kXcds);
+  const int local = (int)(blockIdx.x / kXcds);
+  const int k = local / ntq;
+  const int tq = ntq - 1 - (local - k * ntq);
+  const int pair = xcd + kXcds * k;
+  if (pair >= npairs) return;
   const int b = pair / p.hkv, g = pair - b * p.hkv;
 
   const int tok0 = p.cu_seqlens[b];
@@ -509,8 +513,8 @@ hipError_t launch_prefill(const PrefillParams &p, hipStream_t stream) {
   if (p.ns <= 0 || p.max_chunk_len <= 0 || p.total_tokens <= 0) return hipSuccess;
   const int npos = kRows / p.group;
   const int64_t ntq = (p.max_chunk_len + npos - 1) / npos;
-  const int64_t total = ntq * p.ns * p.hkv;
-  const int64_t grid = (total + kXcds - 1) / kXcds * kXcds;
+  const int64_t pairs_per_xcd = ((int64_t)p.ns * p.hkv + kXcds - 1) / kXcds;
+  const int64_t grid = pairs_per_xcd * ntq * kXcds;
   return launch_kernel(prefill_kernel, dim3((unsigned)grid), dim3(kThreads), stream, p);
 }
 
