@@ -749,8 +749,8 @@ def extra_reports(wl, full_avg):
     for _ in range(3):
         mt.step()
     torch.cuda.synchronize()
-    mt_full = mt.time_kind("full")
-    mt_swa = mt.time_kind("swa")
+    mt_full = mt.time_kind_back_to_back("full", 20)
+    mt_swa = mt.time_kind_back_to_back("swa", 20)
     mtp = {"queries_per_seq": 4, "full_ms": round(mt_full, 5), "swa_ms": round(mt_swa, 5),
            "full_gbs": round(mt.bytes["full"] / (mt_full * 1e-3) / 1e9, 1),
            "full_ms_vs_one_query": round(mt_full / full_avg, 3)}

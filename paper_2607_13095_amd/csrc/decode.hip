@@ -78,10 +78,14 @@ struct Chunk {
 template <bool kSplit>
 constexpr int kWaves = kSplit ? 4 : 1;
 
-// At most 168 VGPRs, so that three waves share a SIMD.
-template <bool kSplit, bool kOnePage>
-__global__ __launch_bounds__(kWave * kWaves<kSplit>) __attribute__((amdgpu_waves_per_eu(3))) void decode_kernel(
-    DecodeParams p) {
+// kCGd: 16-column MFMA groups per wave. With one group (a single query, or
+// few query heads) a wave has at most 168 VGPRs, so that three waves share a
+// SIMD. With two groups (several queries: 32 (query, head) columns of a KV
+// head) one wave scores both against the same K/V loads, which halves the KV
+// bytes read; its accumulators double, so two waves share a SIMD.
+template <bool kSplit, bool kOnePage, int kCGd>
+__global__ __launch_bounds__(kWave * kWaves<kSplit>) __attribute__((amdgpu_waves_per_eu(kCGd == 1 ? 3 : 2))) void
+decode_kernel(DecodeParams p) {
   const PoolView &pv = p.pool;
   const int lane = threadIdx.x & (kWave - 1);
   const int64_t item = (int64_t)blockIdx.x * kWaves<kSplit> + (threadIdx.x >> 6);
@@ -91,7 +95,7 @@ __global__ __launch_bounds__(kWave * kWaves<kSplit>) __attribute__((amdgpu_waves
   const int pg = 1 << shift;
   const float c2 = p.scale_log2;
   const int ncols = p.nq * p.group;  // (query, head) pairs of one KV head
-  const int hchunks = (ncols + kCols - 1) / kCols;
+  const int hchunks = (ncols + kCols * kCGd - 1) / (kCols * kCGd);  // column items per KV head
 
   // Loop-invariant byte offsets of this lane's operands inside one 32-key K
   // block (used when a 32-key chunk never straddles two pages, i.e. PG >= 32):
@@ -147,19 +151,31 @@ __global__ __launch_bounds__(kWave * kWaves<kSplit>) __attribute__((amdgpu_waves
   {
     const int g = gy / hchunks;
     const int hc = gy - g * hchunks;
-    // this lane's MFMA column: query qi of the sequence, head hh of KV head g's group
-    const int col = hc * kCols + r;
-    const bool colv = col < ncols;
-    const int qi = colv ? col / p.group : 0;
-    const int hh = colv ? col - qi * p.group : 0;
-    const int64_t row = ((int64_t)b * p.nq + qi) * p.hq + (int64_t)g * p.group + hh;  // output row (if colv)
+    // this lane's MFMA column in group cg: query qi of the sequence, head hh of
+    // KV head g's group
+    int qi[kCGd];
+    bool colv[kCGd];
+    int64_t row[kCGd];  // output rows (where colv)
+#pragma unroll
+    for (int cg = 0; cg < kCGd; ++cg) {
+      const int col = (hc * kCGd + cg) * kCols + r;
+      colv[cg] = col < ncols;
+      qi[cg] = colv[cg] ? col / p.group : 0;
+      const int hh = colv[cg] ? col - qi[cg] * p.group : 0;
+      row[cg] = ((int64_t)b * p.nq + qi[cg]) * p.hq + (int64_t)g * p.group + hh;
+    }
 
     const int ctx = min(p.ctx_lens[b], p.max_ctx);
     if (ctx < 1) {
-      if (!kSplit && colv) {
+      if (!kSplit) {
         const u32x2 z = {0u, 0u};
 #pragma unroll
-        for (int dt = 0; dt < 8; ++dt) *reinterpret_cast<u32x2 *>(p.out + row * kHeadDim + 16 * dt + 4 * q) = z;
+        for (int cg = 0; cg < kCGd; ++cg)
+          if (colv[cg]) {
+#pragma unroll
+            for (int dt = 0; dt < 8; ++dt)
+              *reinterpret_cast<u32x2 *>(p.out + row[cg] * kHeadDim + 16 * dt + 4 * q) = z;
+          }
       }
       return;
     }
@@ -173,20 +189,25 @@ __global__ __launch_bounds__(kWave * kWaves<kSplit>) __attribute__((amdgpu_waves
       kb = pv.window > 0 ? max(0, pos0 - pv.window + 1) : 0;
       ke = pos;
     }
-    // keys this lane's column may see: causal among the queries, and its own window
-    const int cpos = pos0 + qi;
-    const int ckb = max(kb, pv.window > 0 ? max(0, cpos - pv.window + 1) : 0);
-    const int cke = min(ke, cpos);
+    // keys this lane's columns may see: causal among the queries, and their window
+    int ckb[kCGd], cke[kCGd];
+#pragma unroll
+    for (int cg = 0; cg < kCGd; ++cg) {
+      const int cpos = pos0 + qi[cg];
+      ckb[cg] = max(kb, pv.window > 0 ? max(0, cpos - pv.window + 1) : 0);
+      cke[cg] = min(ke, cpos);
+    }
 
-    // Q^T operand: lane holds column r, dims 32t + 8q .. +7 for step t.
-    u32x4 qf[4];
-    {
-      const uint16_t *qrow = p.q + (colv ? row : (int64_t)b * p.nq * p.hq) * kHeadDim;
+    // Q^T operands: lane holds column r of group cg, dims 32t + 8q .. +7 for step t.
+    u32x4 qf[kCGd][4];
+#pragma unroll
+    for (int cg = 0; cg < kCGd; ++cg) {
+      const uint16_t *qrow = p.q + (colv[cg] ? row[cg] : (int64_t)b * p.nq * p.hq) * kHeadDim;
 #pragma unroll
       for (int t = 0; t < 4; ++t) {
         const u32x4 v = ldg128(qrow + 32 * t + 8 * q);
         const u32x4 z = {0u, 0u, 0u, 0u};
-        qf[t] = colv ? v : z;
+        qf[cg][t] = colv[cg] ? v : z;
       }
     }
 
@@ -198,12 +219,17 @@ __global__ __launch_bounds__(kWave * kWaves<kSplit>) __attribute__((amdgpu_waves
     LaneTable tab;
     load_lane_table(tab, pv, b, kb >> shift, last_lp, lane);
 
-    // Running column maximum: finite start, raised lazily (see scores).
-    float m = -FLT_MAX, lsum = 0.f;
+    // Running column maxima: finite start, raised lazily (see scores).
+    float m[kCGd], lsum[kCGd];
     const float thresh = kRescaleLog2 / c2;  // in raw score units
-    f32x4 acc[8];
+    f32x4 acc[kCGd][8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int cg = 0; cg < kCGd; ++cg) {
+      m[cg] = -FLT_MAX;
+      lsum[cg] = 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) acc[cg][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
 
     auto issue_k = [&](int c, int page, Chunk &ch) {
       const int cbase = cfirst + c * kChunk;
@@ -268,58 +294,64 @@ __global__ __launch_bounds__(kWave * kWaves<kSplit>) __attribute__((amdgpu_waves
     // a masked score (-inf) gives probability 0 without (-inf) - (-inf), and
     // the first finite score always raises the maximum (alpha = 0).
     uint32_t keep = 0;
-    auto scores = [&](Chunk &ch) {
-      f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = {0.f, 0.f, 0.f, 0.f};
+    auto scores = [&](Chunk &ch, u32x4 (&pf)[kCGd]) {
+      f32x4 sa[kCGd], sb[kCGd];
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        sa = mfma16x16x32(ch.ka[t], qf[t], sa);
-        sb = mfma16x16x32(ch.kb[t], qf[t], sb);
-      }
+      for (int cg = 0; cg < kCGd; ++cg) sa[cg] = sb[cg] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int cg = 0; cg < kCGd; ++cg) {
+          sa[cg] = mfma16x16x32(ch.ka[t], qf[cg][t], sa[cg]);
+          sb[cg] = mfma16x16x32(ch.kb[t], qf[cg][t], sb[cg]);
+        }
       // keep: keys of the item range (V rows outside it are zeroed below);
       // sk: those this lane's column sees
       keep = 0;
-      uint32_t sk = 0;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        keep |= (uint32_t)(ch.kv0 + i >= kb && ch.kv0 + i <= ke) << i;
-        sk |= (uint32_t)(ch.kv0 + i >= ckb && ch.kv0 + i <= cke) << i;
-      }
+      for (int i = 0; i < 8; ++i) keep |= (uint32_t)(ch.kv0 + i >= kb && ch.kv0 + i <= ke) << i;
       if (!ch.vok) keep = 0;
-      sk &= keep;
-      float s[8];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        s[i] = (sk >> i) & 1u ? sa[i] : -INFINITY;
-        s[4 + i] = (sk >> (4 + i)) & 1u ? sb[i] : -INFINITY;
+      for (int cg = 0; cg < kCGd; ++cg) {
+        uint32_t sk = 0;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) sk |= (uint32_t)(ch.kv0 + i >= ckb[cg] && ch.kv0 + i <= cke[cg]) << i;
+        sk &= keep;
+        float s[8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          s[i] = (sk >> i) & 1u ? sa[cg][i] : -INFINITY;
+          s[4 + i] = (sk >> (4 + i)) & 1u ? sb[cg][i] : -INFINITY;
+        }
+        const float lmax = max8(s);
+        if (__builtin_amdgcn_ballot_w64(lmax > m[cg] + thresh) != 0) {
+          const float cmax = max_xor32(max_xor16(lmax));
+          const bool up = cmax > m[cg] + thresh;
+          const float alpha = up ? fast_exp2((m[cg] - cmax) * c2) : 1.f;
+          m[cg] = up ? cmax : m[cg];
+          lsum[cg] *= alpha;
+#pragma unroll
+          for (int dt = 0; dt < 8; ++dt) acc[cg][dt] *= alpha;
+        }
+        const float mc = m[cg] * c2;
+        float pr[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) pr[i] = fast_exp2(fmaf(s[i], c2, -mc));
+#pragma unroll
+        for (int j = 0; j < 4; ++j) pf[cg][j] = pack_bf16x2(pr[2 * j], pr[2 * j + 1]);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) lsum[cg] = dot2_bf16_ones(pf[cg][j], lsum[cg]);
       }
-      const float lmax = max8(s);
-      if (__builtin_amdgcn_ballot_w64(lmax > m + thresh) != 0) {
-        const float cmax = max_xor32(max_xor16(lmax));
-        const bool up = cmax > m + thresh;
-        const float alpha = up ? fast_exp2((m - cmax) * c2) : 1.f;
-        m = up ? cmax : m;
-        lsum *= alpha;
-#pragma unroll
-        for (int dt = 0; dt < 8; ++dt) acc[dt] *= alpha;
-      }
-      const float mc = m * c2;
-      float pr[8];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) pr[i] = fast_exp2(fmaf(s[i], c2, -mc));
-      u32x4 pf;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) pf[j] = pack_bf16x2(pr[2 * j], pr[2 * j + 1]);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) lsum = dot2_bf16_ones(pf[j], lsum);
-      return pf;
     };
-    auto pv_update = [&](Chunk &ch, u32x4 pf) {
+    auto pv_update = [&](Chunk &ch, const u32x4 (&pf)[kCGd]) {
       if (keep != 0xFFu) {
 #pragma unroll
         for (int dt = 0; dt < 8; ++dt) ch.v[dt] = keep_bf16x8(ch.v[dt], keep);
       }
 #pragma unroll
-      for (int dt = 0; dt < 8; ++dt) acc[dt] = mfma16x16x32(ch.v[dt], pf, acc[dt]);
+      for (int dt = 0; dt < 8; ++dt)
+#pragma unroll
+        for (int cg = 0; cg < kCGd; ++cg) acc[cg][dt] = mfma16x16x32(ch.v[dt], pf[cg], acc[cg][dt]);
     };
 
     // The one-page path needs every page of the range in the lane table; the
@@ -336,9 +368,10 @@ __global__ __launch_bounds__(kWave * kWaves<kSplit>) __attribute__((amdgpu_waves
       }
       // The scheduling fences keep each chunk's loads behind the last use of
       // the registers they overwrite: one operand set, no loop-carried copies.
+      u32x4 pf[kCGd];
       for (int c = 0; c < nchunks - 1; ++c) {
         const int next_page = page_of(c + 1);
-        const u32x4 pf = scores(ch);
+        scores(ch, pf);
         __builtin_amdgcn_sched_barrier(0);
         issue_k(c + 1, next_page, ch);
         __builtin_amdgcn_sched_barrier(0);
@@ -347,35 +380,38 @@ __global__ __launch_bounds__(kWave * kWaves<kSplit>) __attribute__((amdgpu_waves
         issue_v(c + 1, next_page, ch);
         __builtin_amdgcn_sched_barrier(0);
       }
-      const u32x4 pf = scores(ch);
+      scores(ch, pf);
       pv_update(ch, pf);
     } else {
       for (int c = 0; c < nchunks; ++c) {
         Chunk ch;
+        u32x4 pf[kCGd];
         issue(c, ch);
-        const u32x4 pf = scores(ch);
+        scores(ch, pf);
         pv_update(ch, pf);
       }
     }
 
-    // Normalise and write: lane holds O^T[d = 16 dt + 4 q + i][head r].
-    lsum = sum_xor32(sum_xor16(lsum));
-    if (colv) {
+    // Normalise and write: lane holds O^T[d = 16 dt + 4 q + i][column r of group cg].
+#pragma unroll
+    for (int cg = 0; cg < kCGd; ++cg) {
+      const float l = sum_xor32(sum_xor16(lsum[cg]));
+      if (!colv[cg]) continue;
       // a column that sees no key of this piece (a later query's last keys)
       // writes o = 0 with log-sum-exp -inf: weight 0 in the merge
-      const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
+      const float inv = l > 0.f ? 1.f / l : 0.f;
       if (kSplit) {
-        float *dst = p.ws_o + (row * p.max_splits + split) * kHeadDim + 4 * q;
+        float *dst = p.ws_o + (row[cg] * p.max_splits + split) * kHeadDim + 4 * q;
 #pragma unroll
-        for (int dt = 0; dt < 8; ++dt) *reinterpret_cast<f32x4 *>(dst + 16 * dt) = acc[dt] * inv;
-        if (q == 0) p.ws_lse[row * p.max_splits + split] = m * c2 + __log2f(lsum);
+        for (int dt = 0; dt < 8; ++dt) *reinterpret_cast<f32x4 *>(dst + 16 * dt) = acc[cg][dt] * inv;
+        if (q == 0) p.ws_lse[row[cg] * p.max_splits + split] = m[cg] * c2 + __log2f(l);
       } else {
-        uint16_t *dst = p.out + row * kHeadDim + 4 * q;
+        uint16_t *dst = p.out + row[cg] * kHeadDim + 4 * q;
 #pragma unroll
         for (int dt = 0; dt < 8; ++dt) {
           u32x2 w;
-          w[0] = pack_bf16x2(acc[dt][0] * inv, acc[dt][1] * inv);
-          w[1] = pack_bf16x2(acc[dt][2] * inv, acc[dt][3] * inv);
+          w[0] = pack_bf16x2(acc[cg][dt][0] * inv, acc[cg][dt][1] * inv);
+          w[1] = pack_bf16x2(acc[cg][dt][2] * inv, acc[cg][dt][3] * inv);
           *reinterpret_cast<u32x2 *>(dst + 16 * dt) = w;
         }
       }
@@ -467,10 +503,10 @@ int32_t decode_split_len(int32_t ns, int32_t hkv, int32_t group, int32_t max_ctx
   return len;
 }
 
-hipError_t launch_decode(const DecodeParams &p, hipStream_t stream) {
-  if (p.ns <= 0) return hipSuccess;
-  const int hchunks = (p.nq * p.group + kCols - 1) / kCols;
-  const int64_t items = (int64_t)p.ns * p.hkv * hchunks * p.max_splits;  // upper bound
+template <int kCGd>
+hipError_t launch_decode_cg(const DecodeParams &p, hipStream_t stream) {
+  const int hitems = (p.nq * p.group + kCols * kCGd - 1) / (kCols * kCGd);
+  const int64_t items = (int64_t)p.ns * p.hkv * hitems * p.max_splits;  // upper bound
   const unsigned grid4 = (unsigned)((items + kWaves<true> - 1) / kWaves<true>);
   const unsigned grid1 = (unsigned)items;
   // One-page path: 32-key chunks never straddle pages (PG >= 32) and every key
@@ -481,8 +517,8 @@ hipError_t launch_decode(const DecodeParams &p, hipStream_t stream) {
   const bool one_page = p.pool.pg_shift >= 5 && range_pages < kWave;
   if (p.max_splits > 1) {
     const dim3 block(kWave * kWaves<true>);
-    const hipError_t e = one_page ? launch_kernel(decode_kernel<true, true>, dim3(grid4), block, stream, p)
-                                  : launch_kernel(decode_kernel<true, false>, dim3(grid4), block, stream, p);
+    const hipError_t e = one_page ? launch_kernel(decode_kernel<true, true, kCGd>, dim3(grid4), block, stream, p)
+                                  : launch_kernel(decode_kernel<true, false, kCGd>, dim3(grid4), block, stream, p);
     if (e != hipSuccess) return e;
     const int64_t rows = (int64_t)p.ns * p.nq * p.hq;
     const int per_block = kMergeThreads / kWave;
@@ -490,8 +526,14 @@ hipError_t launch_decode(const DecodeParams &p, hipStream_t stream) {
                          dim3(kMergeThreads), stream, p);
   }
   const dim3 block(kWave * kWaves<false>);
-  return one_page ? launch_kernel(decode_kernel<false, true>, dim3(grid1), block, stream, p)
-                  : launch_kernel(decode_kernel<false, false>, dim3(grid1), block, stream, p);
+  return one_page ? launch_kernel(decode_kernel<false, true, kCGd>, dim3(grid1), block, stream, p)
+                  : launch_kernel(decode_kernel<false, false, kCGd>, dim3(grid1), block, stream, p);
+}
+
+hipError_t launch_decode(const DecodeParams &p, hipStream_t stream) {
+  if (p.ns <= 0) return hipSuccess;
+  // more than 16 (query, head) columns per KV head: one wave takes 32 of them
+  return p.nq * p.group > kCols ? launch_decode_cg<2>(p, stream) : launch_decode_cg<1>(p, stream);
 }
 
 }  // namespace hswa
