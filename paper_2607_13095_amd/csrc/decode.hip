@@ -72,11 +72,15 @@ struct Chunk {
   bool vok;
 };
 
-// Waves (independent items) per workgroup: four for split pieces (thousands of
-// items), one for whole ranges (an SWA layer has only sequences x head groups
-// items, which four-wave workgroups would spread over too few CUs).
+// A workgroup holds four waves. Split pieces (thousands of items): each wave
+// runs an item of its own. Whole ranges (an SWA window, or a FULL context of
+// one piece: only sequences x head groups items, each a short chain of
+// dependent chunk loads): the four waves share one item, take every fourth
+// chunk of its range, and combine their partial softmax states through LDS
+// (still one pass: no workspace and no second kernel).
+constexpr int kWaves = 4;
 template <bool kSplit>
-constexpr int kWaves = kSplit ? 4 : 1;
+constexpr int kCoop = kSplit ? 1 : kWaves;  // waves that share one item
 
 // kCGd: 16-column MFMA groups per wave. With one group (a single query, or
 // few query heads) a wave has at most 168 VGPRs, so that three waves share a
@@ -84,11 +88,12 @@ constexpr int kWaves = kSplit ? 4 : 1;
 // head) one wave scores both against the same K/V loads, which halves the KV
 // bytes read; its accumulators double, so two waves share a SIMD.
 template <bool kSplit, bool kOnePage, int kCGd>
-__global__ __launch_bounds__(kWave * kWaves<kSplit>) __attribute__((amdgpu_waves_per_eu(kCGd == 1 ? 3 : 2))) void
+__global__ __launch_bounds__(kWave * kWaves) __attribute__((amdgpu_waves_per_eu(kCGd == 1 ? 3 : 2))) void
 decode_kernel(DecodeParams p) {
   const PoolView &pv = p.pool;
   const int lane = threadIdx.x & (kWave - 1);
-  const int64_t item = (int64_t)blockIdx.x * kWaves<kSplit> + (threadIdx.x >> 6);
+  const int wid = threadIdx.x >> 6;  // wave of the workgroup
+  const int64_t item = kSplit ? (int64_t)blockIdx.x * kWaves + wid : (int64_t)blockIdx.x;
   const int r = lane & 15, q = lane >> 4;
   const int hkv = p.hkv;
   const int shift = pv.pg_shift;
@@ -167,7 +172,7 @@ decode_kernel(DecodeParams p) {
 
     const int ctx = min(p.ctx_lens[b], p.max_ctx);
     if (ctx < 1) {
-      if (!kSplit) {
+      if (!kSplit && wid == 0) {
         const u32x2 z = {0u, 0u};
 #pragma unroll
         for (int cg = 0; cg < kCGd; ++cg)
@@ -213,6 +218,7 @@ decode_kernel(DecodeParams p) {
 
     const int cfirst = kb & ~(kChunk - 1);
     const int nchunks = ((ke - cfirst) >> 5) + 1;
+    const int c0 = kSplit ? 0 : wid;  // first chunk of this wave
     const int klo8 = kb & ~7, khi8 = ke & ~7;
     const int last_lp = ke >> shift;
 
@@ -360,30 +366,35 @@ decode_kernel(DecodeParams p) {
       auto page_of = [&](int c) {
         return __builtin_amdgcn_readlane(tab.page, ((cfirst + c * kChunk) >> shift) - tab.lp0);
       };
-      Chunk ch;
-      {
-        const int page = page_of(0);
-        issue_k(0, page, ch);
-        issue_v(0, page, ch);
-      }
-      // The scheduling fences keep each chunk's loads behind the last use of
-      // the registers they overwrite: one operand set, no loop-carried copies.
-      u32x4 pf[kCGd];
-      for (int c = 0; c < nchunks - 1; ++c) {
-        const int next_page = page_of(c + 1);
+      // this wave's chunks: c0, c0 + kCoop, ...
+      const int nw = nchunks > c0 ? (nchunks - c0 + kCoop<kSplit> - 1) / kCoop<kSplit> : 0;
+      if (nw > 0) {
+        Chunk ch;
+        {
+          const int page = page_of(c0);
+          issue_k(c0, page, ch);
+          issue_v(c0, page, ch);
+        }
+        // The scheduling fences keep each chunk's loads behind the last use of
+        // the registers they overwrite: one operand set, no loop-carried copies.
+        u32x4 pf[kCGd];
+        for (int k = 0; k < nw - 1; ++k) {
+          const int cn = c0 + (k + 1) * kCoop<kSplit>;
+          const int next_page = page_of(cn);
+          scores(ch, pf);
+          __builtin_amdgcn_sched_barrier(0);
+          issue_k(cn, next_page, ch);
+          __builtin_amdgcn_sched_barrier(0);
+          pv_update(ch, pf);
+          __builtin_amdgcn_sched_barrier(0);
+          issue_v(cn, next_page, ch);
+          __builtin_amdgcn_sched_barrier(0);
+        }
         scores(ch, pf);
-        __builtin_amdgcn_sched_barrier(0);
-        issue_k(c + 1, next_page, ch);
-        __builtin_amdgcn_sched_barrier(0);
         pv_update(ch, pf);
-        __builtin_amdgcn_sched_barrier(0);
-        issue_v(c + 1, next_page, ch);
-        __builtin_amdgcn_sched_barrier(0);
       }
-      scores(ch, pf);
-      pv_update(ch, pf);
     } else {
-      for (int c = 0; c < nchunks; ++c) {
+      for (int c = c0; c < nchunks; c += kCoop<kSplit>) {
         Chunk ch;
         u32x4 pf[kCGd];
         issue(c, ch);
@@ -392,28 +403,69 @@ decode_kernel(DecodeParams p) {
       }
     }
 
-    // Normalise and write: lane holds O^T[d = 16 dt + 4 q + i][column r of group cg].
+    // Lane holds O^T[d = 16 dt + 4 q + i][column r of group cg], relative to
+    // its column maximum m.
+    if constexpr (!kSplit) {
+      // Combine the kCoop waves' partial states through LDS; wave w then
+      // normalises and writes dims 32 w .. 32 w + 31 of every column.
+      // s_o keeps each lane's accumulator vectors in lane order (16-B stores and
+      // loads, no bank conflicts)
+      __shared__ f32x4 s_o[kCoop<kSplit>][kCGd][8][kWave];
+      __shared__ float s_m[kCoop<kSplit>][kCGd][kCols], s_l[kCoop<kSplit>][kCGd][kCols];
 #pragma unroll
-    for (int cg = 0; cg < kCGd; ++cg) {
-      const float l = sum_xor32(sum_xor16(lsum[cg]));
-      if (!colv[cg]) continue;
-      // a column that sees no key of this piece (a later query's last keys)
-      // writes o = 0 with log-sum-exp -inf: weight 0 in the merge
-      const float inv = l > 0.f ? 1.f / l : 0.f;
-      if (kSplit) {
+      for (int cg = 0; cg < kCGd; ++cg) {
+        const float l = sum_xor32(sum_xor16(lsum[cg]));
+        if (q == 0) {
+          s_m[wid][cg][r] = m[cg];
+          s_l[wid][cg][r] = l;
+        }
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) s_o[wid][cg][dt][lane] = acc[cg][dt];
+      }
+      __syncthreads();
+      // this lane's 8 output dims d0 .. d0 + 7: dims 16 dt + 4 q' + i of the
+      // accumulators with dt = 2 wid + q / 2 and q' = 2 (q % 2), 2 (q % 2) + 1
+      const int d0 = 32 * wid + 8 * q;
+      const int sdt = 2 * wid + (q >> 1), sl = r + 32 * (q & 1);
+#pragma unroll
+      for (int cg = 0; cg < kCGd; ++cg) {
+        if (!colv[cg]) continue;
+        float mx = -FLT_MAX;
+#pragma unroll
+        for (int w = 0; w < kCoop<kSplit>; ++w) mx = fmaxf(mx, s_m[w][cg][r]);
+        float wgt[kCoop<kSplit>], l = 0.f;
+#pragma unroll
+        for (int w = 0; w < kCoop<kSplit>; ++w) {
+          wgt[w] = fast_exp2((s_m[w][cg][r] - mx) * c2);
+          l += wgt[w] * s_l[w][cg][r];
+        }
+        // a column that sees no key at all (a query before position 0) writes zeros
+        const float inv = l > 0.f ? 1.f / l : 0.f;
+        f32x4 o0 = {0.f, 0.f, 0.f, 0.f}, o1 = o0;
+#pragma unroll
+        for (int w = 0; w < kCoop<kSplit>; ++w) {
+          o0 += wgt[w] * s_o[w][cg][sdt][sl];
+          o1 += wgt[w] * s_o[w][cg][sdt][sl + 16];
+        }
+        const float o[8] = {o0[0] * inv, o0[1] * inv, o0[2] * inv, o0[3] * inv,
+                            o1[0] * inv, o1[1] * inv, o1[2] * inv, o1[3] * inv};
+        u32x4 wv;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) wv[j] = pack_bf16x2(o[2 * j], o[2 * j + 1]);
+        *reinterpret_cast<u32x4 *>(p.out + row[cg] * kHeadDim + d0) = wv;
+      }
+    } else {
+#pragma unroll
+      for (int cg = 0; cg < kCGd; ++cg) {
+        const float l = sum_xor32(sum_xor16(lsum[cg]));
+        if (!colv[cg]) continue;
+        // a column that sees no key of this piece (a later query's last keys)
+        // writes o = 0 with log-sum-exp -inf: weight 0 in the merge
+        const float inv = l > 0.f ? 1.f / l : 0.f;
         float *dst = p.ws_o + (row[cg] * p.max_splits + split) * kHeadDim + 4 * q;
 #pragma unroll
         for (int dt = 0; dt < 8; ++dt) *reinterpret_cast<f32x4 *>(dst + 16 * dt) = acc[cg][dt] * inv;
         if (q == 0) p.ws_lse[row[cg] * p.max_splits + split] = m[cg] * c2 + __log2f(l);
-      } else {
-        uint16_t *dst = p.out + row[cg] * kHeadDim + 4 * q;
-#pragma unroll
-        for (int dt = 0; dt < 8; ++dt) {
-          u32x2 w;
-          w[0] = pack_bf16x2(acc[cg][dt][0] * inv, acc[cg][dt][1] * inv);
-          w[1] = pack_bf16x2(acc[cg][dt][2] * inv, acc[cg][dt][3] * inv);
-          *reinterpret_cast<u32x2 *>(dst + 16 * dt) = w;
-        }
       }
     }
   }
@@ -507,8 +559,8 @@ template <int kCGd>
 hipError_t launch_decode_cg(const DecodeParams &p, hipStream_t stream) {
   const int hitems = (p.nq * p.group + kCols * kCGd - 1) / (kCols * kCGd);
   const int64_t items = (int64_t)p.ns * p.hkv * hitems * p.max_splits;  // upper bound
-  const unsigned grid4 = (unsigned)((items + kWaves<true> - 1) / kWaves<true>);
-  const unsigned grid1 = (unsigned)items;
+  const unsigned grid4 = (unsigned)((items + kWaves - 1) / kWaves);  // split: one item per wave
+  const unsigned grid1 = (unsigned)items;                             // whole range: one item per workgroup
   // One-page path: 32-key chunks never straddle pages (PG >= 32) and every key
   // range fits the 64-entry lane table.
   const int64_t range = p.max_splits > 1 ? p.split_len
@@ -516,7 +568,7 @@ hipError_t launch_decode_cg(const DecodeParams &p, hipStream_t stream) {
   const int64_t range_pages = ((range + (1 << p.pool.pg_shift) - 1) >> p.pool.pg_shift) + 1;
   const bool one_page = p.pool.pg_shift >= 5 && range_pages < kWave;
   if (p.max_splits > 1) {
-    const dim3 block(kWave * kWaves<true>);
+    const dim3 block(kWave * kWaves);
     const hipError_t e = one_page ? launch_kernel(decode_kernel<true, true, kCGd>, dim3(grid4), block, stream, p)
                                   : launch_kernel(decode_kernel<true, false, kCGd>, dim3(grid4), block, stream, p);
     if (e != hipSuccess) return e;
@@ -525,7 +577,7 @@ hipError_t launch_decode_cg(const DecodeParams &p, hipStream_t stream) {
     return launch_kernel(decode_merge_kernel, dim3((unsigned)((rows + per_block - 1) / per_block)),
                          dim3(kMergeThreads), stream, p);
   }
-  const dim3 block(kWave * kWaves<false>);
+  const dim3 block(kWave * kWaves);
   return one_page ? launch_kernel(decode_kernel<false, true, kCGd>, dim3(grid1), block, stream, p)
                   : launch_kernel(decode_kernel<false, false, kCGd>, dim3(grid1), block, stream, p);
 }
