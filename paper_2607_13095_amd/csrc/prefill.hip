@@ -9,19 +9,20 @@
 // Work unit: one workgroup (8 waves, two per SIMD) per (tile of 256 query rows,
 // KV head, sequence). A query row is a (position, query head) pair of the KV
 // head's GQA group, so one K/V tile in LDS serves every query head that shares
-// it. Each wave owns 32 rows (two 16-column MFMA groups); two waves per SIMD
-// let one wave's softmax run while the other's matrix products do. Per 64-key
-// tile:
+// it. Each wave owns 32 rows (two 16-column MFMA groups). Per 64-key tile:
 //   S^T[key][row]  = K[key][:] . Q[row][:]          (bf16 MFMA, fp32 accumulate)
 //   online softmax per row in fp32 (exp2, scale*log2(e) folded in); the running
 //   maximum is only raised when a score exceeds it by more than 2^8 in exp2
 //   units, so the output rescale is rare (exact: numerator and denominator share
 //   the stale maximum)
 //   O^T[d][row]   += V^T[d][key] . P^T[key][row]    (bf16 MFMA)
-// K is staged in LDS as rows (in the order the MFMA rows consume them), V as its
-// transpose, both with padded rows so that the 16 lanes reading one operand hit
-// distinct banks; four LDS tile buffers let tile j+3 be stored while tiles j and
-// j+1 are read, and the global loads of tile j+4 are in flight meanwhile.
+// The two waves of a SIMD play ping-pong: while one runs its matrix products
+// (QK^T of one tile, PV of the previous one) the other runs its softmax and
+// stages tiles, and workgroup barriers swap the roles, so the matrix cores and
+// the vector ALUs work at the same time.
+// LDS holds the tiles in MFMA operand order (every operand read is one
+// contiguous, conflict-free 1 KiB); four tile buffers let two tiles be read
+// while a third is stored, and the global loads of a fourth are in flight.
 // Keys outside the workgroup's range are staged as zeros, so NaN or stale data
 // in unused cache slots never reaches an accumulator; per-element masks are
 // applied only on tiles that cross the causal diagonal, the window edge or the
@@ -41,19 +42,30 @@ constexpr int kRows = 256;  // query rows per workgroup
 constexpr int kKT = 64;     // keys per tile
 constexpr int kCG = 2;      // 16-column MFMA groups per wave
 constexpr int kXcds = 8;
-constexpr int kBufs = 4;  // LDS tile buffers: two being read, one written, one spare
+constexpr int kBufs = 4;  // LDS tile buffers: two being read, one stored, one loading
 constexpr float kRescaleLog2 = 8.f;
-// LDS rows are padded by 16 bytes, so the 16 lanes that read one MFMA operand
-// (16 consecutive LDS rows at one column) spread over all banks, and every
-// address of a wave's operand reads is a per-lane base plus a constant.
-constexpr int kKRow = kHeadDim + 8;  // K tile row (one key), in bf16 elements
-constexpr int kVRow = kKT + 8;       // V^T tile row (one dim), in bf16 elements
+constexpr int kAhead = 6;  // LDS operand reads in flight ahead of the matrix products
+// LDS holds each tile in MFMA operand order: every operand a wave reads (K: 16
+// keys x 32 dims of a QK^T step; V^T: 16 dims x 32 keys of a PV step) is a
+// contiguous 1 KiB block with lane l's 16 bytes at 16 l, so each operand read
+// is one conflict-free ds_read_b128 at a per-lane base plus a constant.
+//   K tile: block (h, ab, t) at ((2 h + ab) * 4 + t) KiB holds, for lane
+//     r + 16 q, dims 32 t + 8 q .. +7 of tile key 32 h + 8 (r >> 2) + 4 ab + (r & 3):
+//     MFMA row r of the QK^T step of half h, block ab, dim slab t. This is the
+//     pool's K block layout, so an interior tile is a straight copy.
+//   V^T tile: block (h, dt) at 16 KiB + (8 h + dt) KiB holds, for lane r + 16 q,
+//     keys 32 h + 8 q .. +7 of dim 16 dt + r.
+constexpr int kKTileBytes = kKT * kHeadDim * 2;
+constexpr int kBufBytes = 2 * kKTileBytes;
 
-// LDS row of key k (0..63) of a tile: the MFMA row that consumes it. Within each
-// 32-key half, keys 8a+c (c < 4) feed row 4a+c of block a (rows 0..15) and keys
-// 8a+4+c feed row 4a+c of block b (rows 16..31).
-__device__ __forceinline__ int k_lds_row(int k) {
-  return (k & 32) | ((k & 4) << 2) | ((k >> 3 & 3) << 2) | (k & 3);
+// LDS byte offset (within a K tile) of dims 8 c .. +7 of tile key k.
+__device__ __forceinline__ uint32_t k_lds_off(int k, int c) {
+  const int h = k >> 5, ab = (k >> 2) & 1, r = (((k >> 3) & 3) << 2) | (k & 3);
+  return (uint32_t)((((2 * h + ab) * 4 + (c >> 2)) * 64 + r + 16 * (c & 3)) * 16);
+}
+// LDS byte offset (within a buffer) of keys 32 h + 8 q .. +7 of dim d (V^T).
+__device__ __forceinline__ uint32_t v_lds_off(int h, int q, int d) {
+  return (uint32_t)(kKTileBytes + ((8 * h + (d >> 4)) * 64 + (d & 15) + 16 * q) * 16);
 }
 
 __device__ __forceinline__ int64_t prefix_page(const PoolView &pv, int b, int key, bool &ok) {
@@ -68,8 +80,6 @@ __device__ __forceinline__ int64_t prefix_page(const PoolView &pv, int b, int ke
   return ok ? page : 0;
 }
 
-constexpr int kKTileBytes = kKT * kKRow * 2;
-constexpr int kBufBytes = kKTileBytes + kHeadDim * kVRow * 2;
 constexpr int kStage = kKT * kHeadDim / 8 / kThreads;  // 16-byte pieces per thread per tile (K or V)
 static_assert(kStage == 2 && kKT == 64, "V staging maps piece i of a thread to 32-key block i");
 
@@ -79,20 +89,19 @@ static_assert(kStage == 2 && kKT == 64, "V staging maps piece i of a thread to 3
 // K tile pieces in pool order: piece idx (0 .. 1023) is 16-byte piece idx & 511
 // of the tile's 32-key block idx >> 9 (half (idx >> 8) & 1, slab (idx >> 6) & 3,
 // dim piece (idx >> 4) & 3, row idx & 15 of the block's K layout), i.e. dims
-// 8 k_piece_c .. +7 of tile key k_piece_key, which LDS holds in row k_piece_row.
+// 8 k_piece_c .. +7 of tile key k_piece_key. LDS holds it at byte 16 idx.
 __device__ __forceinline__ int k_piece_key(int idx) {
   const int r = idx & 15;
   return ((idx >> 9) << 5) | ((r >> 2) << 3) | (((idx >> 8) & 1) << 2) | (r & 3);
 }
 __device__ __forceinline__ int k_piece_c(int idx) { return ((idx >> 6) & 3) * 4 + ((idx >> 4) & 3); }
-__device__ __forceinline__ int k_piece_row(int idx) { return ((idx >> 8) << 4) | (idx & 15); }
 
 __device__ __forceinline__ int v_piece_dim(int tid) { return tid >> 2; }
 __device__ __forceinline__ int v_piece_keys(int tid, int i) { return 4 * i + (tid & 3); }
 
 struct Stage {
   u32x4 k[kStage], v[kStage];
-  bool vrow;  // v[] holds 8 dims of one key (as k[]) instead of 8 keys of one dim
+  bool vrow;  // chunk tile: k[] holds key rows, v[] pieces follow the chunk mapping
 };
 
 __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
@@ -131,7 +140,8 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   const int khi = plast;
 
   const int tid = threadIdx.x;
-  const int lane = tid & (kWave - 1), wave = tid / kWave;
+  const int lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);  // uniform in a wave
   const int r = lane & 15, q = lane >> 4;
   const int hkv = p.hkv, hq = p.hq;
   const int shift = pv.pg_shift, pg = 1 << shift;
@@ -221,18 +231,26 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
     }
     st.vrow = false;
   };
-  // Chunk tile: every key is one of this chunk's own (key >= P), so its K and
-  // V rows are 256-byte runs of k_new / v_new: both are loaded as 16-byte
-  // pieces of a key's row, and V is transposed on its way into LDS.
+  // Chunk tile: every key is one of this chunk's own (key >= P). K and V rows
+  // are 256-byte runs of k_new / v_new, loaded as 16-byte pieces of a row. K
+  // piece i of thread tid is key 32 i + tid / 16, dims 8 (tid % 16) .. +7. V
+  // piece i of lane l of wave w is key 8 w + 4 i + l / 16, dims
+  // 8 (l % 16) .. +7; the store transposes those into V^T (store_tile).
   auto load_tile_chunk = [&](int kt, Stage &st) {
+    const u32x4 z = {0u, 0u, 0u, 0u};
 #pragma unroll
     for (int i = 0; i < kStage; ++i) {
       const int idx = tid + kThreads * i;
       const int j = kt + (idx >> 4);
       const bool in = j >= klo && j <= khi;
       const int64_t off = ((int64_t)(tok0 + (in ? j - P : 0)) * hkv + g) * kHeadDim + (idx & 15) * 8;
-      const u32x4 z = {0u, 0u, 0u, 0u};
       st.k[i] = in ? ldg128(p.k_new + off) : z;
+    }
+#pragma unroll
+    for (int i = 0; i < kStage; ++i) {
+      const int j = kt + 8 * wave + 4 * i + (lane >> 4);
+      const bool in = j >= klo && j <= khi;
+      const int64_t off = ((int64_t)(tok0 + (in ? j - P : 0)) * hkv + g) * kHeadDim + (lane & 15) * 8;
       st.v[i] = in ? ldg128(p.v_new + off) : z;
     }
     st.vrow = true;
@@ -259,30 +277,52 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   // immediate offset field.
   auto buf_off = [&](int buf) { return (uint32_t)__builtin_amdgcn_readfirstlane(buf * kBufBytes); };
   auto lds128 = [&](uint32_t off) { return reinterpret_cast<u32x4 *>(s_lds + off); };
-  // K piece 0 of this thread in pool order (cached tiles) or row order (chunk
-  // tiles); piece 1 is 32 rows on in both.
-  const uint32_t st_k0 = (k_piece_row(tid) * kKRow + k_piece_c(tid) * 8) * 2;
-  const uint32_t st_k0_row = (k_lds_row(tid >> 4) * kKRow + (tid & 15) * 8) * 2;
-  const uint32_t st_v0 = kKTileBytes + (v_piece_dim(tid) * kVRow + v_piece_keys(tid, 0) * 8) * 2;
-  const uint32_t st_vrow0 = kKTileBytes + ((tid & 15) * 8 * kVRow + (tid >> 4)) * 2;  // row form, piece 0
+  // LDS offsets of this thread's pieces. Cached tiles: pool order, piece 1 is
+  // the next 32 keys, 8 KiB on. Chunk tiles: K piece 0 of key tid / 16 (piece
+  // 1: 32 keys on, 8 KiB on); V^T pieces of dims 8 (l % 16) + 2 m and + 1
+  // (m = l / 16), keys 8 w .. +7 (16 bytes apart).
+  const uint32_t st_k0 = tid * 16;
+  const uint32_t st_k0_row = k_lds_off(tid >> 4, tid & 15);
+  const uint32_t st_v0 = v_lds_off(0, v_piece_keys(tid, 0), v_piece_dim(tid));
+  const uint32_t st_vrow0 = v_lds_off(wave >> 2, wave & 3, 8 * (lane & 15) + 2 * (lane >> 4));
+  // 4 x 4 transpose of dwords across the lanes l, l ^ 16, l ^ 32, l ^ 48: the
+  // lane in 16-lane row m enters with dword j of its row m in t[j] and leaves
+  // with dword m of rows 0..3 in w[0..3] (a swap with l ^ 32, then with l ^ 16).
+  auto transpose4 = [&](const u32x4 &t, uint32_t (&w)[4]) {
+    const auto a = __builtin_amdgcn_permlane32_swap(t[0], t[2], false, false);
+    const auto b = __builtin_amdgcn_permlane32_swap(t[1], t[3], false, false);
+    const auto c = __builtin_amdgcn_permlane16_swap((uint32_t)a[0], (uint32_t)b[0], false, false);
+    const auto d = __builtin_amdgcn_permlane16_swap((uint32_t)a[1], (uint32_t)b[1], false, false);
+    w[0] = (uint32_t)c[0];
+    w[1] = (uint32_t)c[1];
+    w[2] = (uint32_t)d[0];
+    w[3] = (uint32_t)d[1];
+  };
   auto store_tile = [&](int buf, const Stage &st) {
     static_assert(kStage == 2, "two pieces per thread");
     const uint32_t bo = buf_off(buf);
-    // piece 1 of K is key + 32 (LDS row + 32), of V keys + 32 (block 1)
     const uint32_t k0 = st.vrow ? st_k0_row : st_k0;
     *lds128(bo + k0) = st.k[0];
-    *lds128(bo + k0 + 32 * kKRow * 2) = st.k[1];
+    *lds128(bo + k0 + kKTileBytes / 2) = st.k[1];
     if (!st.vrow) {
       *lds128(bo + st_v0) = st.v[0];
-      *lds128(bo + st_v0 + 32 * 2) = st.v[1];
+      *lds128(bo + st_v0 + kKTileBytes / 2) = st.v[1];
     } else {
-      // dims 8c .. 8c+7 of key tid/16 (+32 for piece 1): one 2-byte store per dim
+      // The lanes l % 16 + 16 m (m = 0..3) of a wave hold an 8 x 8 block: keys
+      // 8 w + 4 i + m (piece i) x dims 8 (l % 16) .. +7. After the transposes
+      // lane m holds dims 2 m, 2 m + 1 of keys 8 w .. +7 (w[k]); byte permutes
+      // split them into one V^T piece per dim.
+      uint32_t w[8];
+      transpose4(st.v[0], *reinterpret_cast<uint32_t(*)[4]>(&w[0]));
+      transpose4(st.v[1], *reinterpret_cast<uint32_t(*)[4]>(&w[4]));
+      u32x4 lo, hi;
 #pragma unroll
-      for (int i = 0; i < kStage; ++i)
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-          *reinterpret_cast<uint16_t *>(s_lds + bo + st_vrow0 + (e * kVRow + 32 * i) * 2) =
-              (uint16_t)(st.v[i][e >> 1] >> (16 * (e & 1)));
+      for (int j = 0; j < 4; ++j) {
+        lo[j] = __builtin_amdgcn_perm(w[2 * j + 1], w[2 * j], 0x05040100u);
+        hi[j] = __builtin_amdgcn_perm(w[2 * j + 1], w[2 * j], 0x07060302u);
+      }
+      *lds128(bo + st_vrow0) = lo;
+      *lds128(bo + st_vrow0 + 16) = hi;
     }
   };
 
@@ -341,11 +381,9 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   };
 
   // QK^T of one half tile: S^T for keys kt + 32h .. +31.
-  const uint32_t qk_lane = (r * kKRow + 8 * q) * 2;
-  const uint32_t pv_lane = kKTileBytes + (r * kVRow + 8 * q) * 2;
+  const uint32_t op_lane = lane * 16;
   auto qk_half = [&](int buf, int h, f32x4 (&sc)[2][kCG]) {
-    // MFMA row r of block a is LDS row 32h + r, of block b row 32h + 16 + r
-    const uint32_t a = buf_off(buf) + qk_lane + 32 * h * kKRow * 2;
+    const uint32_t a = buf_off(buf) + op_lane + h * (kKTileBytes / 2);
 #pragma unroll
     for (int cg = 0; cg < kCG; ++cg) {
       sc[0][cg] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -353,8 +391,8 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
     }
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      const u32x4 ka = *lds128(a + 64 * t);
-      const u32x4 kb = *lds128(a + 16 * kKRow * 2 + 64 * t);
+      const u32x4 ka = *lds128(a + 1024 * t);
+      const u32x4 kb = *lds128(a + 4096 + 1024 * t);
 #pragma unroll
       for (int cg = 0; cg < kCG; ++cg) {
         sc[0][cg] = mfma16x16x32(ka, qf[cg][t], sc[0][cg]);
@@ -381,21 +419,26 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   auto needs_mask = [&](int kt) {
     return kt + kKT - 1 > pfirst || kt < klo || kt + kKT - 1 > khi || (W > 0 && kt < plast - W + 1);
   };
-  // Lazy raise of the running maximum. Each lane compares the maximum of its
-  // own 8 scores with m + thresh; only if some lane exceeds it (a ballot) is
-  // the exact column maximum formed across the 4 lanes that share a column
-  // and the output rescaled. Otherwise every probability stays below 2^8.
-  // The running maximum starts at -FLT_MAX, a finite value: exp2 of a masked
-  // score (-inf) is then 0 with no NaN from (-inf) - (-inf), and the first
-  // finite score always raises it (alpha = exp2(-huge) = 0).
-  auto softmax_max = [&](f32x4 (&sc)[2][kCG]) {
+  // Lazy raise of the running maximum, over a whole tile. Each lane compares
+  // the maximum of its own 16 scores of a column with m + thresh; only if some
+  // lane exceeds it (a ballot) is the exact column maximum formed across the 4
+  // lanes that share a column and the output rescaled. Otherwise every
+  // probability stays below 2^8. The running maximum starts at -FLT_MAX, a
+  // finite value: exp2 of a masked score (-inf) is then 0 with no NaN from
+  // (-inf) - (-inf), and the first finite score always raises it
+  // (alpha = exp2(-huge) = 0).
+  // The exponentials then give the bf16 P^T operands; the row sums use the same
+  // bf16-rounded probabilities as the PV product.
+  auto softmax_tile = [&](f32x4 (&sc)[2][2][kCG], u32x4 (&pf)[2][kCG]) {
     float lmax[kCG];
     bool raise = false;
 #pragma unroll
     for (int cg = 0; cg < kCG; ++cg) {
-      const float v8[8] = {sc[0][cg][0], sc[0][cg][1], sc[0][cg][2], sc[0][cg][3],
-                           sc[1][cg][0], sc[1][cg][1], sc[1][cg][2], sc[1][cg][3]};
-      lmax[cg] = max8(v8);
+      const float a8[8] = {sc[0][0][cg][0], sc[0][0][cg][1], sc[0][0][cg][2], sc[0][0][cg][3],
+                           sc[0][1][cg][0], sc[0][1][cg][1], sc[0][1][cg][2], sc[0][1][cg][3]};
+      const float b8[8] = {sc[1][0][cg][0], sc[1][0][cg][1], sc[1][0][cg][2], sc[1][0][cg][3],
+                           sc[1][1][cg][0], sc[1][1][cg][1], sc[1][1][cg][2], sc[1][1][cg][3]};
+      lmax[cg] = max2(max8(a8), max8(b8));
       raise = raise || lmax[cg] > m[cg] + thresh;
     }
     if (__builtin_amdgcn_ballot_w64(raise) != 0) {
@@ -410,29 +453,27 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
         for (int dt = 0; dt < 8; ++dt) acc[cg][dt] *= alpha;
       }
     }
-  };
-  // exp2 and the bf16 P^T operand; the row sums use the same bf16-rounded
-  // probabilities as the PV product.
-  auto softmax_exp = [&](f32x4 (&sc)[2][kCG], u32x4 (&pf)[kCG]) {
 #pragma unroll
-    for (int cg = 0; cg < kCG; ++cg) {
-      const float mc = m[cg] * c2;
-      float pr[8];
+    for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int ab = 0; ab < 2; ++ab)
+      for (int cg = 0; cg < kCG; ++cg) {
+        const float mc = m[cg] * c2;
+        float pr[8];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) pr[4 * ab + i] = fast_exp2(fmaf(sc[ab][cg][i], c2, -mc));
+        for (int ab = 0; ab < 2; ++ab)
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) pf[cg][jj] = pack_bf16x2(pr[2 * jj], pr[2 * jj + 1]);
+          for (int i = 0; i < 4; ++i) pr[4 * ab + i] = fast_exp2(fmaf(sc[h][ab][cg][i], c2, -mc));
 #pragma unroll
-      for (int jj = 0; jj < 4; ++jj) lsum[cg] = dot2_bf16_ones(pf[cg][jj], lsum[cg]);
-    }
+        for (int jj = 0; jj < 4; ++jj) pf[h][cg][jj] = pack_bf16x2(pr[2 * jj], pr[2 * jj + 1]);
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) lsum[cg] = dot2_bf16_ones(pf[h][cg][jj], lsum[cg]);
+      }
   };
   // O^T += V^T P^T for one half tile.
   auto load_v = [&](int buf, int h, u32x4 (&vf)[8]) {
-    const uint32_t a = buf_off(buf) + pv_lane + 64 * h;  // keys 32h + 8q .. +7
+    const uint32_t a = buf_off(buf) + kKTileBytes + op_lane + h * (kKTileBytes / 2);  // keys 32h + 8q .. +7
 #pragma unroll
-    for (int dt = 0; dt < 8; ++dt) vf[dt] = *lds128(a + 16 * dt * kVRow * 2);
+    for (int dt = 0; dt < 8; ++dt) vf[dt] = *lds128(a + 1024 * dt);
   };
   auto pv_ops = [&](const u32x4 (&vf)[8], const u32x4 (&pf)[kCG]) {
 #pragma unroll
@@ -441,7 +482,39 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
       for (int cg = 0; cg < kCG; ++cg) acc[cg][dt] = mfma16x16x32(vf[dt], pf[cg], acc[cg][dt]);
   };
 
-  // Prologue: tiles 0..2 in LDS, tile 3's loads in flight, QK^T of (0, 0).
+  // ---- ping-pong tile loop ----
+  // The waves form two groups, A (waves 0-3) and B (waves 4-7), one wave of
+  // each on every SIMD. A tile is processed in two phases separated by
+  // workgroup barriers: a matrix phase (QK^T of tile j and PV of tile j-1,
+  // both on MFMA, operands from LDS, plus this thread's share of the tile
+  // staging) and a softmax phase (VALU only). Group B runs one phase behind
+  // group A, so on every SIMD one wave's matrix products run while the other
+  // wave's exponentials do.
+  //
+  // Phase numbering: A runs the matrix phase of tile j in phase 2j and its
+  // softmax in 2j+1; B one phase later. Tile t is read in phases 2t..2t+3
+  // (K by A then B, V by A then B one tile later). The staging of the tiles
+  // (LDS stores, global loads, address arithmetic) runs in the softmax phases,
+  // which have the slack, so the matrix phases issue little else than MFMAs
+  // and their operand reads: each thread stores its share of tile t in its
+  // softmax phase of tile t-2 (phases 2t-3 and 2t-2), which a barrier
+  // separates from the first read (2t) and from the last read of the tile
+  // that used the buffer before (tile t-4: phase 2t-5). The global loads of a
+  // tile go out one tile before its store.
+  auto phase_barrier = [&]() {
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  auto pv_tile = [&](int buf, const u32x4 (&pf)[2][kCG]) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      u32x4 vf[8];
+      load_v(buf, h, vf);
+      pv_ops(vf, pf[h]);
+    }
+  };
+
   Stage st;
   fetch(kt0, tile_page(kt0), st);
   store_tile(0, st);
@@ -449,44 +522,51 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
     fetch(kt0 + kKT, tile_page(kt0 + kKT), st);
     store_tile(1, st);
   }
-  if (ntiles > 2) {
-    fetch(kt0 + 2 * kKT, tile_page(kt0 + 2 * kKT), st);
-    store_tile(2, st);
-  }
-  if (ntiles > 3) fetch(kt0 + 3 * kKT, tile_page(kt0 + 3 * kKT), st);
+  if (ntiles > 2) fetch(kt0 + 2 * kKT, tile_page(kt0 + 2 * kKT), st);
   __syncthreads();
-  f32x4 s_a[2][kCG], s_b[2][kCG];
-  qk_half(0, 0, s_a);
+  const bool lag = wave >= kThreads / kWave / 2;  // group B
+  if (lag) phase_barrier();
 
+  f32x4 sc[2][2][kCG];
+  u32x4 pf[2][kCG];
   for (int jt = 0; jt < ntiles; ++jt) {
     const int kt = kt0 + jt * kKT;
     const int buf = jt % kBufs;
-    const bool masked = needs_mask(kt);
-    u32x4 pf[kCG], vf[8];
-    // softmax of (jt, 0) with the QK^T of (jt, 1) issued alongside, PV of (jt, 0)
-    load_v(buf, 0, vf);
-    if (masked) mask_half(kt, 0, s_a);
-    softmax_max(s_a);
-    qk_half(buf, 1, s_b);
-    softmax_exp(s_a, pf);
-    pv_ops(vf, pf);
-    // Every wave is past its last read of tile jt-1: tile jt+3 (in registers
-    // since the previous iteration) overwrites its buffer, and tile jt+4's
-    // loads go out, a whole iteration ahead of their store.
-    __syncthreads();
-    if (jt + 3 < ntiles) store_tile((jt + 3) % kBufs, st);
-    if (jt + 4 < ntiles) fetch(kt + 4 * kKT, tile_page(kt + 4 * kKT), st);
-    // softmax of (jt, 1) with the QK^T of (jt + 1, 0) issued alongside (it is
-    // unconditional so that it interleaves with the exponentials; after the
-    // last tile it reads a stale buffer and the result is never used), PV of
-    // (jt, 1)
-    load_v(buf, 1, vf);
-    if (masked) mask_half(kt, 1, s_b);
-    softmax_max(s_b);
-    qk_half((jt + 1) % kBufs, 0, s_a);
-    softmax_exp(s_b, pf);
-    pv_ops(vf, pf);
+    // matrix phase: PV of tile jt-1, QK^T of tile jt
+    if (jt > 0) {
+      pv_tile((jt + kBufs - 1) % kBufs, pf);
+      // operand reads run kAhead reads ahead of the products that use them
+      __builtin_amdgcn_sched_group_barrier(0x100, kAhead, 0);
+#pragma unroll
+      for (int i = 0; i < 16 - kAhead; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 2 * kAhead, 0);
+    }
+    qk_half(buf, 0, sc[0]);
+    qk_half(buf, 1, sc[1]);
+    __builtin_amdgcn_sched_group_barrier(0x100, kAhead, 1);
+#pragma unroll
+    for (int i = 0; i < 16 - kAhead; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 1);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 2 * kAhead, 1);
+    phase_barrier();
+    // softmax phase, with this thread's share of the staging: tile jt+2 from
+    // registers to LDS, tile jt+3's global loads
+    if (jt + 2 < ntiles) store_tile((jt + 2) % kBufs, st);
+    if (jt + 3 < ntiles) fetch(kt + 3 * kKT, tile_page(kt + 3 * kKT), st);
+    if (needs_mask(kt)) {
+      mask_half(kt, 0, sc[0]);
+      mask_half(kt, 1, sc[1]);
+    }
+    softmax_tile(sc, pf);
+    phase_barrier();
   }
+  pv_tile((ntiles + kBufs - 1) % kBufs, pf);
+  if (!lag) phase_barrier();  // every wave passes the same number of barriers
 
   // ---- normalise and write ----
 #pragma unroll
