@@ -58,11 +58,6 @@ constexpr int kAhead = 6;  // LDS operand reads in flight ahead of the matrix pr
 constexpr int kKTileBytes = kKT * kHeadDim * 2;
 constexpr int kBufBytes = 2 * kKTileBytes;
 
-// LDS byte offset (within a K tile) of dims 8 c .. +7 of tile key k.
-__device__ __forceinline__ uint32_t k_lds_off(int k, int c) {
-  const int h = k >> 5, ab = (k >> 2) & 1, r = (((k >> 3) & 3) << 2) | (k & 3);
-  return (uint32_t)((((2 * h + ab) * 4 + (c >> 2)) * 64 + r + 16 * (c & 3)) * 16);
-}
 // LDS byte offset (within a buffer) of keys 32 h + 8 q .. +7 of dim d (V^T).
 __device__ __forceinline__ uint32_t v_lds_off(int h, int q, int d) {
   return (uint32_t)(kKTileBytes + ((8 * h + (d >> 4)) * 64 + (d & 15) + 16 * q) * 16);
@@ -83,9 +78,13 @@ __device__ __forceinline__ int64_t prefix_page(const PoolView &pv, int b, int ke
 constexpr int kStage = kKT * kHeadDim / 8 / kThreads;  // 16-byte pieces per thread per tile (K or V)
 static_assert(kStage == 2 && kKT == 64, "V staging maps piece i of a thread to 32-key block i");
 
-// V^T tile staging: piece i of thread tid holds dim tid / 4 and keys
-// 8 * (4 i + tid % 4) .. +7 of the tile, which in the pool is the 16 bytes at
-// element 8 * tid of the tile's 32-key block i.
+// Staging maps every wave's 16-byte LDS stores onto one contiguous 1 KiB
+// operand block (lane l at 16 l), so the stores are free of bank conflicts;
+// thread tid (lane l of wave w) stores piece i at byte 16 tid + 8 KiB i of the
+// K tile and of the V^T tile.
+// V^T piece i of thread tid: dim 16 w + l % 16, keys 8 (4 i + l / 16) .. +7 of
+// the tile, i.e. piece l / 16 of dim row 16 w + l % 16 of the pool's 32-key V
+// block i (a wave reads one contiguous 1 KiB of the block).
 // K tile pieces in pool order: piece idx (0 .. 1023) is 16-byte piece idx & 511
 // of the tile's 32-key block idx >> 9 (half (idx >> 8) & 1, slab (idx >> 6) & 3,
 // dim piece (idx >> 4) & 3, row idx & 15 of the block's K layout), i.e. dims
@@ -96,8 +95,8 @@ __device__ __forceinline__ int k_piece_key(int idx) {
 }
 __device__ __forceinline__ int k_piece_c(int idx) { return ((idx >> 6) & 3) * 4 + ((idx >> 4) & 3); }
 
-__device__ __forceinline__ int v_piece_dim(int tid) { return tid >> 2; }
-__device__ __forceinline__ int v_piece_keys(int tid, int i) { return 4 * i + (tid & 3); }
+__device__ __forceinline__ int v_piece_dim(int tid) { return 16 * (tid >> 6) + (tid & 15); }
+__device__ __forceinline__ int v_piece_keys(int tid, int i) { return 4 * i + ((tid >> 4) & 3); }
 
 struct Stage {
   u32x4 k[kStage], v[kStage];
@@ -233,17 +232,20 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   };
   // Chunk tile: every key is one of this chunk's own (key >= P). K and V rows
   // are 256-byte runs of k_new / v_new, loaded as 16-byte pieces of a row. K
-  // piece i of thread tid is key 32 i + tid / 16, dims 8 (tid % 16) .. +7. V
-  // piece i of lane l of wave w is key 8 w + 4 i + l / 16, dims
-  // 8 (l % 16) .. +7; the store transposes those into V^T (store_tile).
+  // piece i of lane l of wave w is MFMA row l % 16 of K block (h = i,
+  // ab = w / 4, slab w % 4), dims 32 (w % 4) + 8 (l / 16) .. +7, so it lands at
+  // the same LDS byte as a pool piece. V piece i of lane l of wave w is key
+  // 8 w + 4 i + l / 16, dims 8 (l % 16) .. +7; the store transposes those into
+  // V^T (store_tile).
   auto load_tile_chunk = [&](int kt, Stage &st) {
     const u32x4 z = {0u, 0u, 0u, 0u};
+    const int r = lane & 15, ab = wave >> 2;
 #pragma unroll
     for (int i = 0; i < kStage; ++i) {
-      const int idx = tid + kThreads * i;
-      const int j = kt + (idx >> 4);
+      const int j = kt + 32 * i + 8 * (r >> 2) + 4 * ab + (r & 3);
       const bool in = j >= klo && j <= khi;
-      const int64_t off = ((int64_t)(tok0 + (in ? j - P : 0)) * hkv + g) * kHeadDim + (idx & 15) * 8;
+      const int c = 4 * (wave & 3) + (lane >> 4);
+      const int64_t off = ((int64_t)(tok0 + (in ? j - P : 0)) * hkv + g) * kHeadDim + c * 8;
       st.k[i] = in ? ldg128(p.k_new + off) : z;
     }
 #pragma unroll
@@ -268,7 +270,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
     for (int i = 0; i < kStage; ++i) {
       const int idx = tid + kThreads * i;
       st.k[i] = ldg128(kbase + idx * 8);
-      st.v[i] = ldg128(vbase + i * (32 * kHeadDim) + tid * 8);
+      st.v[i] = ldg128(vbase + i * (32 * kHeadDim) + v_piece_dim(tid) * 32 + ((tid >> 4) & 3) * 8);
     }
     st.vrow = false;
   };
@@ -277,13 +279,11 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   // immediate offset field.
   auto buf_off = [&](int buf) { return (uint32_t)__builtin_amdgcn_readfirstlane(buf * kBufBytes); };
   auto lds128 = [&](uint32_t off) { return reinterpret_cast<u32x4 *>(s_lds + off); };
-  // LDS offsets of this thread's pieces. Cached tiles: pool order, piece 1 is
-  // the next 32 keys, 8 KiB on. Chunk tiles: K piece 0 of key tid / 16 (piece
-  // 1: 32 keys on, 8 KiB on); V^T pieces of dims 8 (l % 16) + 2 m and + 1
-  // (m = l / 16), keys 8 w .. +7 (16 bytes apart).
+  // LDS offsets of this thread's pieces: piece 1 is 8 KiB after piece 0, except
+  // for the V^T pieces of a chunk tile, dims 8 (l % 16) + 2 m and + 1
+  // (m = l / 16) of keys 8 w .. +7, which are 16 bytes apart.
   const uint32_t st_k0 = tid * 16;
-  const uint32_t st_k0_row = k_lds_off(tid >> 4, tid & 15);
-  const uint32_t st_v0 = v_lds_off(0, v_piece_keys(tid, 0), v_piece_dim(tid));
+  const uint32_t st_v0 = kKTileBytes + tid * 16;
   const uint32_t st_vrow0 = v_lds_off(wave >> 2, wave & 3, 8 * (lane & 15) + 2 * (lane >> 4));
   // 4 x 4 transpose of dwords across the lanes l, l ^ 16, l ^ 32, l ^ 48: the
   // lane in 16-lane row m enters with dword j of its row m in t[j] and leaves
@@ -301,9 +301,8 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   auto store_tile = [&](int buf, const Stage &st) {
     static_assert(kStage == 2, "two pieces per thread");
     const uint32_t bo = buf_off(buf);
-    const uint32_t k0 = st.vrow ? st_k0_row : st_k0;
-    *lds128(bo + k0) = st.k[0];
-    *lds128(bo + k0 + kKTileBytes / 2) = st.k[1];
+    *lds128(bo + st_k0) = st.k[0];
+    *lds128(bo + st_k0 + kKTileBytes / 2) = st.k[1];
     if (!st.vrow) {
       *lds128(bo + st_v0) = st.v[0];
       *lds128(bo + st_v0 + kKTileBytes / 2) = st.v[1];
@@ -532,7 +531,10 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   for (int jt = 0; jt < ntiles; ++jt) {
     const int kt = kt0 + jt * kKT;
     const int buf = jt % kBufs;
-    // matrix phase: PV of tile jt-1, QK^T of tile jt
+    // matrix phase: PV of tile jt-1, QK^T of tile jt, at raised issue priority
+    // so that the other wave's softmax takes the issue slots the matrix
+    // products leave free
+    __builtin_amdgcn_s_setprio(2);
     if (jt > 0) {
       pv_tile((jt + kBufs - 1) % kBufs, pf);
       // operand reads run kAhead reads ahead of the products that use them
@@ -554,6 +556,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 2 * kAhead, 1);
     phase_barrier();
+    __builtin_amdgcn_s_setprio(0);
     // softmax phase, with this thread's share of the staging: tile jt+2 from
     // registers to LDS, tile jt+3's global loads
     if (jt + 2 < ntiles) store_tile((jt + 2) % kBufs, st);
