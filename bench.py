@@ -46,11 +46,11 @@ MFMA_BF16_PEAK_TFLOPS = 2516.6
 # once they change the benchmark reports null until it is measured again.
 MEASURED_TRAFFIC = {
     "decode_full": {"sources": ["decode.hip", "hswa_common.h", "hswa_launch.h"],
-                    "sha256": "3f0627ec68b9ebc5c056137cba415beab5bea967ad1fc4f946905a1391818d35",
-                    "fetch_bytes": 4136497562, "write_bytes": 67865907},
+                    "sha256": "873f206f4cfdfc2377c8edec735bb6399ac92a769bc0ef0c23b317664d435c03",
+                    "fetch_bytes": 4136518460, "write_bytes": 67869005},
     "prefill_full": {"sources": ["prefill.hip", "hswa_common.h", "hswa_launch.h"],
-                     "sha256": "91d1ed39ab605e134f4627b0b54f80812d2ae3891a40369480b9d53066deb479",
-                     "fetch_bytes": 1340659661, "write_bytes": 134217728},
+                     "sha256": "21e0e8d30b9517a3114df45ecb83149a1447765b45096afdaa9e42d09b79b70d",
+                     "fetch_bytes": 453194679, "write_bytes": 134217728},
 }
 
 
