@@ -43,7 +43,9 @@ constexpr int kKT = 64;     // keys per tile
 constexpr int kCG = 2;      // 16-column MFMA groups per wave
 constexpr int kXcds = 8;
 constexpr int kBufs = 4;  // LDS tile buffers: two being read, one stored, one loading
-constexpr float kRescaleLog2 = 8.f;
+// a lane's share (16 probabilities) of a row sum above which the running
+// maximum is raised
+constexpr float kLaneSumLimit = 4096.f;
 constexpr int kAhead = 6;  // LDS operand reads in flight ahead of the matrix products
 // LDS holds each tile in MFMA operand order: every operand a wave reads (K: 16
 // keys x 32 dims of a QK^T step; V^T: 16 dims x 32 keys of a PV step) is a
@@ -145,7 +147,6 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   const int hkv = p.hkv, hq = p.hq;
   const int shift = pv.pg_shift, pg = 1 << shift;
   const float c2 = p.scale_log2;
-  const float thresh = kRescaleLog2 / c2;  // in raw score units
 
   // Q^T operands and the position of each of this lane's columns.
   u32x4 qf[kCG][4];
@@ -418,45 +419,28 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   auto needs_mask = [&](int kt) {
     return kt + kKT - 1 > pfirst || kt < klo || kt + kKT - 1 > khi || (W > 0 && kt < plast - W + 1);
   };
-  // Lazy raise of the running maximum, over a whole tile. Each lane compares
-  // the maximum of its own 16 scores of a column with m + thresh; only if some
-  // lane exceeds it (a ballot) is the exact column maximum formed across the 4
-  // lanes that share a column and the output rescaled. Otherwise every
-  // probability stays below 2^8. The running maximum starts at -FLT_MAX, a
+  // Lazy raise of the running maximum, checked after the fact. The
+  // exponentials of a tile are taken against the running maximum m as it
+  // stands, and each lane adds up its 16 probabilities of a column (its share
+  // of the row sum). Only if some lane's share exceeds 2^12 (a ballot; an
+  // infinite sum counts) is the exact column maximum formed across the 4 lanes
+  // that share a column, m raised to it, the output and the row sum rescaled,
+  // and the tile's exponentials taken again. Otherwise every probability is
+  // below 2^12 and m stays: the result is the same either way, because
+  // numerator and denominator share m, and the 2^12 bound keeps both far
+  // inside the fp32 and bf16 ranges. The running maximum starts at -FLT_MAX, a
   // finite value: exp2 of a masked score (-inf) is then 0 with no NaN from
-  // (-inf) - (-inf), and the first finite score always raises it
-  // (alpha = exp2(-huge) = 0).
-  // The exponentials then give the bf16 P^T operands; the row sums use the same
+  // (-inf) - (-inf), and the first finite score always raises it (its
+  // probability overflows to infinity; alpha = exp2(-huge) = 0).
+  // The exponentials give the bf16 P^T operands; the row sums use the same
   // bf16-rounded probabilities as the PV product.
-  auto softmax_tile = [&](f32x4 (&sc)[2][2][kCG], u32x4 (&pf)[2][kCG]) {
-    float lmax[kCG];
-    bool raise = false;
+  auto tile_exp = [&](f32x4 (&sc)[2][2][kCG], u32x4 (&pf)[2][kCG], float (&ts)[kCG]) {
 #pragma unroll
     for (int cg = 0; cg < kCG; ++cg) {
-      const float a8[8] = {sc[0][0][cg][0], sc[0][0][cg][1], sc[0][0][cg][2], sc[0][0][cg][3],
-                           sc[0][1][cg][0], sc[0][1][cg][1], sc[0][1][cg][2], sc[0][1][cg][3]};
-      const float b8[8] = {sc[1][0][cg][0], sc[1][0][cg][1], sc[1][0][cg][2], sc[1][0][cg][3],
-                           sc[1][1][cg][0], sc[1][1][cg][1], sc[1][1][cg][2], sc[1][1][cg][3]};
-      lmax[cg] = max2(max8(a8), max8(b8));
-      raise = raise || lmax[cg] > m[cg] + thresh;
-    }
-    if (__builtin_amdgcn_ballot_w64(raise) != 0) {
+      const float mc = m[cg] * c2;
+      ts[cg] = 0.f;
 #pragma unroll
-      for (int cg = 0; cg < kCG; ++cg) {
-        const float cmax = max_xor32(max_xor16(lmax[cg]));
-        const bool up = cmax > m[cg] + thresh;
-        const float alpha = up ? fast_exp2((m[cg] - cmax) * c2) : 1.f;
-        m[cg] = up ? cmax : m[cg];
-        lsum[cg] *= alpha;
-#pragma unroll
-        for (int dt = 0; dt < 8; ++dt) acc[cg][dt] *= alpha;
-      }
-    }
-#pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-      for (int cg = 0; cg < kCG; ++cg) {
-        const float mc = m[cg] * c2;
+      for (int h = 0; h < 2; ++h) {
         float pr[8];
 #pragma unroll
         for (int ab = 0; ab < 2; ++ab)
@@ -465,8 +449,35 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj) pf[h][cg][jj] = pack_bf16x2(pr[2 * jj], pr[2 * jj + 1]);
 #pragma unroll
-        for (int jj = 0; jj < 4; ++jj) lsum[cg] = dot2_bf16_ones(pf[h][cg][jj], lsum[cg]);
+        for (int jj = 0; jj < 4; ++jj) ts[cg] = dot2_bf16_ones(pf[h][cg][jj], ts[cg]);
       }
+    }
+  };
+  auto softmax_tile = [&](f32x4 (&sc)[2][2][kCG], u32x4 (&pf)[2][kCG]) {
+    float ts[kCG];
+    tile_exp(sc, pf, ts);
+    bool raise = false;
+#pragma unroll
+    for (int cg = 0; cg < kCG; ++cg) raise = raise || !(ts[cg] <= kLaneSumLimit);
+    if (__builtin_amdgcn_ballot_w64(raise) != 0) {
+#pragma unroll
+      for (int cg = 0; cg < kCG; ++cg) {
+        const float a8[8] = {sc[0][0][cg][0], sc[0][0][cg][1], sc[0][0][cg][2], sc[0][0][cg][3],
+                             sc[0][1][cg][0], sc[0][1][cg][1], sc[0][1][cg][2], sc[0][1][cg][3]};
+        const float b8[8] = {sc[1][0][cg][0], sc[1][0][cg][1], sc[1][0][cg][2], sc[1][0][cg][3],
+                             sc[1][1][cg][0], sc[1][1][cg][1], sc[1][1][cg][2], sc[1][1][cg][3]};
+        const float cmax = max_xor32(max_xor16(max2(max8(a8), max8(b8))));
+        const bool up = cmax > m[cg];
+        const float alpha = up ? fast_exp2((m[cg] - cmax) * c2) : 1.f;
+        m[cg] = up ? cmax : m[cg];
+        lsum[cg] *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) acc[cg][dt] *= alpha;
+      }
+      tile_exp(sc, pf, ts);
+    }
+#pragma unroll
+    for (int cg = 0; cg < kCG; ++cg) lsum[cg] += ts[cg];
   };
   // O^T += V^T P^T for one half tile.
   auto load_v = [&](int buf, int h, u32x4 (&vf)[8]) {
