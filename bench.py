@@ -47,10 +47,10 @@ MFMA_BF16_PEAK_TFLOPS = 2516.6
 MEASURED_TRAFFIC = {
     "decode_full": {"sources": ["decode.hip", "hswa_common.h", "hswa_launch.h"],
                     "sha256": "873f206f4cfdfc2377c8edec735bb6399ac92a769bc0ef0c23b317664d435c03",
-                    "fetch_bytes": 4136518460, "write_bytes": 67869005},
+                    "fetch_bytes": 4136518256, "write_bytes": 67865355},
     "prefill_full": {"sources": ["prefill.hip", "hswa_common.h", "hswa_launch.h"],
-                     "sha256": "21e0e8d30b9517a3114df45ecb83149a1447765b45096afdaa9e42d09b79b70d",
-                     "fetch_bytes": 453194679, "write_bytes": 134217728},
+                     "sha256": "e99e9b0ba317e5d4308a00a8cfcf170fc12cb74f19373b777cb2e512a5459867",
+                     "fetch_bytes": 453225386, "write_bytes": 134217728},
 }
 
 
