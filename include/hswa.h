@@ -189,21 +189,26 @@ hswa_status hswa_prefill(hswa_layer layer, const hswa_shape *shape, const hswa_c
                          int32_t total_tokens, int32_t max_chunk_len, void *out, void *stream);
 
 /* Workspace bytes hswa_decode needs for a FULL layer (0 for an SWA layer is
- * enough): fp32 partial outputs and log-sum-exps of every split-KV piece.
+ * enough): fp32 partial outputs and log-sum-exps of every split-KV piece
+ * (at most ceil(max_context_len / hswa_decode_split_len) + 1 per output row).
  * Returns 0 on an invalid shape. */
 size_t hswa_decode_workspace_bytes(const hswa_shape *shape, int32_t ns, int32_t max_context_len);
 
-/* Keys per split-KV piece that hswa_decode uses for a FULL layer; pieces are
- * [s*len, (s+1)*len) in logical positions, so results do not depend on where
- * pages sit physically. Returns -1 on an invalid shape. */
+/* Fewest keys of a split-KV span that hswa_decode uses for a FULL layer (a
+ * multiple of 256); max_context_len at most this long decodes in one pass.
+ * Returns -1 on an invalid shape. */
 int32_t hswa_decode_split_len(const hswa_shape *shape, int32_t ns, int32_t max_context_len);
 
 /* Decode: one query per sequence at position c_b = context_lens[b] - 1, where
  * context_lens counts the cached tokens including the one just appended
  * ("KVCache Storage Analysis": decode is memory-bound). SWA layers read at most
- * W keys from the ring in a single pass; FULL layers split the context into
- * pieces of hswa_decode_split_len keys, write fp32 partials to the workspace
- * and merge them by log-sum-exp.
+ * W keys from the ring in a single pass. FULL layers cut the 32-key chunks of
+ * all (sequence, KV head) pairs, taken in that order, into equal spans, one per
+ * wave the device holds at once (each at least hswa_decode_split_len keys);
+ * a pair met by several spans gets fp32 partials in the workspace, merged by
+ * log-sum-exp. The cuts are logical positions: results do not depend on where
+ * pages sit physically, but their rounding may depend on the other sequences'
+ * lengths and on the device's compute-unit count.
  * q: device bf16 [ns][Hq][D]; context_lens: device int32 [ns], each in
  * [1, max_context_len] (values above max_context_len are clamped to it, values
  * below 1 give a zero output row); out: device bf16 [ns][Hq][D];

@@ -93,9 +93,13 @@ DecodeGeometry decode_geometry(const hswa_shape *sh, int32_t ns, int32_t max_ctx
   DecodeGeometry g{};
   const int group = sh->num_q_heads / sh->num_kv_heads;
   g.split_len = hswa::decode_split_len(ns, sh->num_kv_heads, group, max_ctx);
-  g.max_splits = (max_ctx + g.split_len - 1) / g.split_len;
-  if (g.max_splits < 1) g.max_splits = 1;
-  if (g.max_splits == 1) return g;  // single pass, no workspace
+  if (max_ctx <= g.split_len) {  // single pass, no workspace
+    g.max_splits = 1;
+    return g;
+  }
+  // a segment of at most max_ctx keys meets at most ceil(max_ctx / split_len) + 1
+  // spans of at least split_len keys
+  g.max_splits = (max_ctx + g.split_len - 1) / g.split_len + 1;
   const size_t rows = (size_t)ns * nq * sh->num_q_heads * g.max_splits;
   g.o_bytes = align_up(rows * sh->head_dim * sizeof(float), 256);
   g.total_bytes = g.o_bytes + align_up(rows * sizeof(float), 256);

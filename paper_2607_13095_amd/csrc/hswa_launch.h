@@ -49,7 +49,10 @@ struct DecodeParams {
   float *ws_lse;          // [ns * nq * Hq][max_splits]
   int32_t ns, hq, hkv, group, max_ctx;
   int32_t nq;             // queries per sequence, at positions ctx - nq .. ctx - 1 (q, out: [ns][nq][Hq][D])
-  int32_t split_len, max_splits;  // max_splits == 1 => single pass, no workspace
+  int32_t split_len;      // FULL split: fewest keys of a wave's span (a multiple of 32)
+  int32_t max_splits;     // pieces a (row) may have; 1 => single pass, no workspace
+  int32_t span_waves;     // FULL split: waves the chunk order is divided over (set at launch)
+  int32_t item_cols;      // (query, head) columns of one item (set at launch)
   float scale_log2;       // scale * log2(e)
 };
 
@@ -69,7 +72,7 @@ hipError_t launch_kv_append(const AppendParams &p, hipStream_t stream);
 hipError_t launch_decode(const DecodeParams &p, hipStream_t stream);
 hipError_t launch_prefill(const PrefillParams &p, hipStream_t stream);
 
-// Split-KV piece length (keys) for a FULL decode; a multiple of 256.
+// Fewest keys of a FULL decode wave's span; a multiple of 256.
 int32_t decode_split_len(int32_t ns, int32_t hkv, int32_t group, int32_t max_ctx);
 
 }  // namespace hswa

@@ -69,21 +69,28 @@ def test_decode_window_one_is_exact_value(gpu_lib):
 
 @pytest.mark.parametrize("pg", [16, 64])
 def test_decode_full_split_boundaries(gpu_lib, pg):
+    """Contexts around multiples of split_len, as one batch and one sequence at
+    a time. Alone, a sequence of few chunks gets spans of exactly split_len
+    keys, so KV head 0's pieces are [s * split_len, (s + 1) * split_len): then a
+    last piece holding only the newest key, quarter pieces and exact
+    boundaries all occur; in the batch the span cuts fall elsewhere."""
     shape = hswa.Shape(64, 8, 128, pg)
     ns = 12
     maxc = 5000
     sl = hswa.decode_split_len(shape, ns, maxc)
     assert sl % 256 == 0 and sl > 0
     tl = sl // 4
-    # contexts (keys incl. the new token, c + 1) at piece boundaries +-1 (the
-    # last piece then holds only the newest key), at quarter pieces, just
-    # below three pieces, shorter than one piece, and the max
     ctxs = [sl - 2, sl - 1, sl, 2 * sl - 1, 2 * sl, sl + tl - 1, sl + tl, 2 * sl + 3 * tl, tl - 1, 3 * sl - 2,
             3 * sl - 1, maxc - 1]
     assert len(ctxs) == ns and max(c + 1 for c in ctxs) == maxc and maxc > sl
     print(f"[decode-full-split] pg={pg} split_len={sl}", flush=True)
     gpu, ref = run_decode("full", 0, pg, 64, 8, ctxs, (203, pg))
     assert_close(gpu, ref, f"full split PG={pg}")
+    for c in ctxs:
+        if c + 1 <= hswa.decode_split_len(shape, 1, c + 1):
+            continue  # one pass
+        gpu, ref = run_decode("full", 0, pg, 64, 8, [c], (203, pg, c))
+        assert_close(gpu, ref, f"full split PG={pg} alone, context {c + 1}")
 
 
 def test_decode_full_long(gpu_lib):
@@ -101,3 +108,63 @@ def test_decode_context_clamp_and_empty(gpu_lib):
     hswa.decode(layer, shape, kv.cache, q, i32([0, -3]), 64, out)
     torch.cuda.synchronize()
     assert torch.count_nonzero(out).item() == 0
+
+
+def test_decode_full_spans_cross_short_segments(gpu_lib):
+    """FULL split over a batch of many short and some long contexts: the spans
+    (about 16 chunks here) cross (sequence, head) segments of 1-13 chunks, so
+    some segments are covered whole by one wave (output written directly) and
+    others are cut into pieces merged by log-sum-exp."""
+    rng = np.random.default_rng(206)
+    ctxs = [int(x) for x in rng.integers(0, 420, size=100)] + [6000] * 12
+    rng.shuffle(ctxs)
+    shape = hswa.Shape(64, 16, 128, 64)
+    sl = hswa.decode_split_len(shape, len(ctxs), max(ctxs) + 1)
+    assert max(ctxs) + 1 > sl  # the split path
+    print(f"[decode-full-spans] ns={len(ctxs)} split_len={sl}", flush=True)
+    gpu, ref = run_decode("full", 0, 64, 64, 16, ctxs, (206,))
+    assert_close(gpu, ref, "full spans over short segments")
+
+
+def test_decode_full_split_with_empty_contexts(gpu_lib):
+    """context_lens < 1 inside a split batch: those rows are zero, the span walk
+    skips them, and every other row matches the oracle."""
+    ctxs = [700, 0, 5000, 3, 0, 2500, 64, 4095]
+    ns = len(ctxs)
+    final = [c + 1 for c in ctxs]
+    shape = hswa.Shape(64, 8, 128, 16)
+    seed = (207,)
+    layer, kv = make_layer("full", 0, shape, final, seed)
+    hist = SeqHistory(final, 8, 128, *seed)
+    append_history(layer, shape, kv, hist, [0] * ns, ctxs)
+    append_history(layer, shape, kv, hist, ctxs, final)
+    qbits = synth.normal_bf16((ns, 64, 128), *seed, synth.TAG_QDEC)
+    lens = [0 if i in (1, 4) else f for i, f in enumerate(final)]
+    lens[6] = -5
+    maxc = max(final)
+    out = torch.full((ns, 64, 128), 3.0, dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(max(1, hswa.decode_workspace_bytes(shape, ns, maxc)), dtype=torch.uint8, device="cuda")
+    assert maxc > hswa.decode_split_len(shape, ns, maxc)
+    print(f"[decode-full-empty] lens={lens}", flush=True)
+    hswa.decode(layer, shape, kv.cache, to_dev(qbits), i32(lens), maxc, out, workspace=ws)
+    torch.cuda.synchronize()
+    gpu = to_f64(out)
+    qf = OA.bf16_bits_to_f64(qbits)
+    for b in range(ns):
+        if lens[b] < 1:
+            assert np.all(gpu[b] == 0.0), b
+        else:
+            ref = OA.decode(qf[b], OA.bf16_bits_to_f64(hist.k[b]), OA.bf16_bits_to_f64(hist.v[b]), None)
+            assert_close(gpu[b], ref, f"full split with empty contexts, row {b}")
+
+
+def test_decode_full_one_long_sequence_many_pieces(gpu_lib):
+    """One 70000-key sequence: its eight head segments are each cut into more
+    than 64 pieces (the merge takes them in several 64-wide passes)."""
+    ctxs = [69999]
+    shape = hswa.Shape(64, 8, 128, 64)
+    sl = hswa.decode_split_len(shape, 1, 70000)
+    assert 70000 / sl > 64
+    print(f"[decode-full-one-long] split_len={sl}", flush=True)
+    gpu, ref = run_decode("full", 0, 64, 64, 8, ctxs, (208,))
+    assert_close(gpu, ref, "full one long sequence")

@@ -65,10 +65,12 @@ def test_decode_multi_groups(gpu_lib, hq, hkv):
 
 
 def test_decode_multi_split_tail(gpu_lib):
-    """FULL pieces: final contexts (c + nq) one past a piece boundary, so the
-    last piece holds only the newest key, which the first three queries do not
-    see; then quarter-piece offsets, an exact boundary, one below three pieces
-    and the max."""
+    """FULL split with final contexts (c + nq) one past a multiple of split_len,
+    quarter offsets, an exact multiple, one below three and the max, as one
+    batch and one sequence at a time. Alone, KV head 0's spans are split_len
+    keys from position 0, so a final context of s * split_len + 1 leaves a last
+    piece holding only the newest key, which the first three queries do not
+    see (their partials carry weight 0 in the merge)."""
     nq, ns, maxc = 4, 7, 6000
     shape = hswa.Shape(64, 8, D, 64)
     sl = hswa.decode_split_len(shape, ns, maxc)
@@ -77,6 +79,12 @@ def test_decode_multi_split_tail(gpu_lib):
     ctxs = [f - nq for f in finals]
     gpu, ref, _ = run_multi("full", 0, 64, 64, 8, ctxs, nq, (902,))
     assert_close(gpu, ref, f"decode multi split tail, split_len {sl}")
+    for f in finals:
+        sl1 = hswa.decode_split_len(shape, 1, f)
+        if f <= sl1:
+            continue  # one pass
+        gpu, ref, _ = run_multi("full", 0, 64, 64, 8, [f - nq], nq, (902, f))
+        assert_close(gpu, ref, f"decode multi split tail alone, final {f}, split_len {sl1}")
 
 
 def test_decode_multi_split_no_visible_key(gpu_lib):
