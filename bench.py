@@ -46,11 +46,11 @@ MFMA_BF16_PEAK_TFLOPS = 2516.6
 # once they change the benchmark reports null until it is measured again.
 MEASURED_TRAFFIC = {
     "decode_full": {"sources": ["decode.hip", "hswa_common.h", "hswa_launch.h"],
-                    "sha256": "873f206f4cfdfc2377c8edec735bb6399ac92a769bc0ef0c23b317664d435c03",
-                    "fetch_bytes": 4136518256, "write_bytes": 67865355},
+                    "sha256": "a3f66ed9d3e531aac9d80aa9c69110a213dbcd93cc88299e96a6bacde1a87893",
+                    "fetch_bytes": 4100957394, "write_bytes": 34749121},
     "prefill_full": {"sources": ["prefill.hip", "hswa_common.h", "hswa_launch.h"],
-                     "sha256": "e99e9b0ba317e5d4308a00a8cfcf170fc12cb74f19373b777cb2e512a5459867",
-                     "fetch_bytes": 453225386, "write_bytes": 134217728},
+                     "sha256": "0f480bc1173720a12440ca104f61931cab2c2ffbe7cd6fb8b16772aa08ca3a76",
+                     "fetch_bytes": 453118809, "write_bytes": 134217728},
 }
 
 
