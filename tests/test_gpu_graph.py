@@ -123,3 +123,55 @@ def test_graph_prefill_replays(gpu_lib):
             assert torch.equal(out.view(torch.int16), eager.view(torch.int16)), f"replay {rep} {kind}"
             call()
             torch.cuda.synchronize()
+
+
+_CAPTURE_FIRST = r"""
+import numpy as np, torch, sys
+sys.path.insert(0, '.')
+import synth
+from paper_2607_13095_amd import hswa
+from tests.hswa_testlib import SeqHistory, append_history, i32, make_layer, to_dev, to_f64
+ctxs = [700, 3000, 5000]
+ns, hq, hkv, D = 3, 32, 4, 128
+final = [c + 1 for c in ctxs]
+maxc = max(final)
+shape = hswa.Shape(hq, hkv, D, 64)
+assert maxc > hswa.decode_split_len(shape, ns, maxc)
+layer, kv = make_layer("full", 0, shape, final, (1102,))
+hist = SeqHistory(final, hkv, D, 1102)
+append_history(layer, shape, kv, hist, [0] * ns, final)
+q = to_dev(synth.normal_bf16((ns, hq, D), 1102, synth.TAG_QDEC))
+ws = torch.empty(max(1, hswa.decode_workspace_bytes(shape, ns, maxc)), dtype=torch.uint8, device="cuda")
+out = torch.zeros((ns, hq, D), dtype=torch.bfloat16, device="cuda")
+lens = i32(final)
+torch.cuda.synchronize()
+g = torch.cuda.CUDAGraph()
+with torch.cuda.graph(g):  # the process's first decode call
+    hswa.decode(layer, shape, kv.cache, q, lens, maxc, out, workspace=ws)
+outs = []
+for _ in range(3):
+    out.zero_()
+    g.replay()
+    torch.cuda.synchronize()
+    outs.append(to_f64(out))
+eager = torch.empty_like(out)
+hswa.decode(layer, shape, kv.cache, q, lens, maxc, eager, workspace=ws)
+torch.cuda.synchronize()
+ref = to_f64(eager)
+assert np.abs(ref).max() > 0
+assert all(np.array_equal(o, ref) for o in outs)
+print("CAPTURE-FIRST OK", flush=True)
+"""
+
+
+def test_graph_capture_is_first_decode_call(gpu_lib):
+    """A FULL (split) decode captured before the process has made any eager
+    decode call: the device's resident wave count, looked up on first use,
+    must be obtainable inside a capture. Runs in a fresh child process."""
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    print("[graph] capture as the first decode call (child process)", flush=True)
+    r = subprocess.run([sys.executable, "-c", _CAPTURE_FIRST], cwd=root, capture_output=True, text=True, timeout=200)
+    assert r.returncode == 0 and "CAPTURE-FIRST OK" in r.stdout, (r.returncode, r.stdout[-2000:], r.stderr[-3000:])
