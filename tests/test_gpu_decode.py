@@ -156,6 +156,11 @@ def test_decode_full_split_with_empty_contexts(gpu_lib):
         else:
             ref = OA.decode(qf[b], OA.bf16_bits_to_f64(hist.k[b]), OA.bf16_bits_to_f64(hist.v[b]), None)
             assert_close(gpu[b], ref, f"full split with empty contexts, row {b}")
+    # every context empty on the split path: no wave has work, the merge zeroes every row
+    out.fill_(3.0)
+    hswa.decode(layer, shape, kv.cache, to_dev(qbits), i32([0] * ns), maxc, out, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(out).item() == 0
 
 
 def test_decode_full_one_long_sequence_many_pieces(gpu_lib):
