@@ -22,7 +22,10 @@
  * Conventions shared by every call
  * ---------------------------------------------------------------------------
  * Ownership. The caller owns every buffer. The library never allocates, frees
- *   or keeps device memory and holds no state between calls; all calls are
+ *   or keeps device memory, and keeps one piece of state
+ *   between calls: per device, the number of waves the FULL decode kernel can
+ *   hold resident, looked up on the first FULL decode call on that device and
+ *   cached (atomically) for the life of the process. All calls are
  *   thread-safe. Pointers marked "device" are device (HBM) addresses, "host"
  *   pointers are read synchronously during the call.
  * Streams. Compute calls enqueue on `stream` (a hipStream_t passed as void*;
@@ -57,9 +60,15 @@
  *                 R = hswa_ring_pages(W, PG); position j lives in ring entry
  *                 (j / PG) mod R at offset j mod PG, so the ring holds the
  *                 latest R*PG positions.
- *   Entries outside [0, num_pages) are never dereferenced: keys on such pages
- *   are treated as absent (the result is then meaningless but no memory
- *   outside the pools is touched).
+ *   Entries outside [0, num_pages), and logical pages at or past
+ *   table_stride, are never dereferenced: no memory outside the pools is
+ *   touched. A key the call needs on such an entry is a caller error whose
+ *   rows come out wrong: hswa_decode leaves the key out, hswa_prefill reads it
+ *   as a zero key and value (score 0, so it still takes part in the softmax).
+ *   hswa_decode checks table_stride * page_size >= max_context_len on the host
+ *   (HSWA_ERR_CAPACITY); hswa_prefill cannot (the prefix lengths live on the
+ *   device), so a FULL or SWA_PAGED table must hold ceil((P_b + C_b) / PG)
+ *   entries per sequence.
  * Ordering. Decode: hswa_kv_append of the new token, then hswa_decode (which
  *   reads the new token from the cache; the ring slot the new token at c
  *   overwrites held position c - R*PG, outside the window since R*PG > W).
@@ -135,10 +144,16 @@ typedef struct {
 int32_t hswa_ring_pages(int32_t window, int32_t page_size);
 
 /* Bytes of one page of one pool (K or V): Hkv * page_size * head_dim * 2.
- * Returns -1 on a null or non-positive shape. */
+ * Pool sizes follow from it ("KVCache Storage Analysis": a FULL layer stores
+ * every position of every sequence, an SWA layer only its window, so an SWA
+ * pool of ns * R pages is flat in the context length). Returns -1 on a null or
+ * non-positive shape. */
 int64_t hswa_page_bytes(const hswa_shape *shape);
 
-/* Fill a block table (host memory) from a permutation of physical page ids:
+/* Fill a block table (host memory) from a permutation of physical page ids
+ * ("KVCache Dual-Pool Design": the FULL index maps a sequence's logical pages
+ * to physical pages, and a separate mapping gives its SWA pages; here the SWA
+ * mapping is the ring of R entries):
  * sequence b needs n_b pages (FULL: ceil(final_lens[b] / page_size); SWA: R)
  * and receives perm[o_b .. o_b + n_b - 1], o_b = n_0 + ... + n_{b-1}; unused
  * entries are -1. table_out is int32 [ns][stride]. Returns HSWA_ERR_CAPACITY
@@ -191,7 +206,10 @@ hswa_status hswa_prefill(hswa_layer layer, const hswa_shape *shape, const hswa_c
 /* Workspace bytes hswa_decode needs for a FULL layer (0 for an SWA layer is
  * enough): fp32 partial outputs and log-sum-exps of every split-KV piece
  * (at most ceil(max_context_len / hswa_decode_split_len) + 1 per output row).
- * Returns 0 on an invalid shape. */
+ * The split exists because decode is memory-bound ("KVCache Storage
+ * Analysis"): a long FULL context is read by many waves at once, and their
+ * pieces are merged by the log-sum-exp identity. Returns 0 on an invalid
+ * shape. */
 size_t hswa_decode_workspace_bytes(const hswa_shape *shape, int32_t ns, int32_t max_context_len);
 
 /* Fewest keys of a split-KV span that hswa_decode uses for a FULL layer (a
@@ -219,7 +237,6 @@ hswa_status hswa_decode(hswa_layer layer, const hswa_shape *shape, const hswa_ca
                         int32_t max_context_len, void *workspace, size_t workspace_bytes,
                         void *out, void *stream);
 
-/* Static string naming a status. */
 /* Multi-query decode ("MTP Optimization": the model verifies 1 + 3 predicted
  * tokens per sequence per step): num_queries (1 .. 64) new queries per
  * sequence at positions c_b - num_queries .. c_b - 1, where c_b =
@@ -227,6 +244,12 @@ hswa_status hswa_decode(hswa_layer layer, const hswa_shape *shape, const hswa_ca
  * first). Query i attends keys lo .. its own position (causal among the new
  * tokens; lo as in hswa_decode for its own position). Queries whose position
  * is negative get zero rows.
+ * SWA limits: the first query reads the W - 1 keys before it, which must
+ * still be cached after all num_queries appends. A ring (HSWA_LAYER_SWA)
+ * keeps the latest R * PG positions, so num_queries <= R * PG - W + 1 (17 at
+ * PG 16 and W 128, 65 at PG 64); an explicit-release table
+ * (HSWA_LAYER_SWA_PAGED) holds the last W positions of one extend, so
+ * num_queries <= W. Larger counts return HSWA_ERR_UNSUPPORTED.
  * q, out: device bf16 [ns][num_queries][Hq][D]; workspace >=
  * hswa_decode_multi_workspace_bytes (FULL only). num_queries = 1 is exactly
  * hswa_decode. */
@@ -237,6 +260,7 @@ hswa_status hswa_decode_multi(hswa_layer layer, const hswa_shape *shape, const h
                               int32_t max_context_len, void *workspace, size_t workspace_bytes, void *out,
                               void *stream);
 
+/* Static string naming a status. */
 const char *hswa_status_string(hswa_status status);
 
 /* ---- explicit-release dual-pool page allocator (host) -------------------

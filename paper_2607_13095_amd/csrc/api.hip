@@ -89,6 +89,20 @@ struct DecodeGeometry {
 
 constexpr int32_t kMaxQueries = 64;  // queries per sequence in one decode call
 
+// The first of nq new queries of an SWA layer reads the W - 1 keys before it,
+// which must still be held once all nq tokens are appended. A ring keeps the
+// latest R * PG positions, so nq <= R * PG - W + 1. An explicit-release table
+// stores only the last W of the positions one extend adds, so nq <= W.
+hswa_status check_multi_window(hswa_layer layer, const hswa_shape *sh, int32_t nq) {
+  if (layer.kind == HSWA_LAYER_SWA) {
+    const int64_t held = (int64_t)hswa_ring_pages(layer.window, sh->page_size) * sh->page_size;
+    if ((int64_t)nq > held - layer.window + 1) return HSWA_ERR_UNSUPPORTED;
+  } else if (layer.kind == HSWA_LAYER_SWA_PAGED) {
+    if (nq > layer.window) return HSWA_ERR_UNSUPPORTED;
+  }
+  return HSWA_OK;
+}
+
 DecodeGeometry decode_geometry(const hswa_shape *sh, int32_t ns, int32_t max_ctx, int32_t nq) {
   DecodeGeometry g{};
   const int group = sh->num_q_heads / sh->num_kv_heads;
@@ -220,6 +234,7 @@ hswa_status hswa_decode_multi(hswa_layer layer, const hswa_shape *shape, const h
   if (ns < 0 || max_context_len < 1 || num_queries < 1 || num_queries > kMaxQueries) return HSWA_ERR_INVALID_ARG;
   hswa::PoolView pv{};
   if ((st = make_pool(layer, shape, cache, pv)) != HSWA_OK) return st;
+  if ((st = check_multi_window(layer, shape, num_queries)) != HSWA_OK) return st;
   // FULL-style tables are indexed by the logical page of every position
   if ((layer.kind == HSWA_LAYER_FULL || layer.kind == HSWA_LAYER_SWA_PAGED) &&
       (int64_t)cache->table_stride * shape->page_size < (int64_t)max_context_len)

@@ -279,9 +279,9 @@ decode_kernel(DecodeParams p) {
       LaneTable tab;
       load_lane_table(tab, pv, b, kb >> shift, last_lp, lane);
 
-      // Running column maxima: finite start, raised lazily (see scores).
+      // Running column maxima in exp2 units (score * scale * log2 e): a finite
+      // start whatever the scale, raised lazily (see scores).
       float m[kCGd], lsum[kCGd];
-      const float thresh = kRescaleLog2 / c2;  // in raw score units
       f32x4 acc[kCGd][8];
 #pragma unroll
       for (int cg = 0; cg < kCGd; ++cg) {
@@ -350,9 +350,10 @@ decode_kernel(DecodeParams p) {
       // raised when one of its scores exceeds it by more than 2^8 in exp2 units
       // (a ballot over the lanes' own maxima; the exact column maximum is formed
       // only then), so the output rescale is rare; numerator and denominator
-      // share the stale maximum, so the result is exact. Starting from -FLT_MAX,
-      // a masked score (-inf) gives probability 0 without (-inf) - (-inf), and
-      // the first finite score always raises the maximum (alpha = 0).
+      // share the stale maximum, so the result is exact. Starting from -FLT_MAX
+      // (exp2 units), a masked score (-inf) gives probability 0 without
+      // (-inf) - (-inf), and the first finite score always raises the maximum
+      // (alpha = 0).
       uint32_t keep = 0;
       auto qk = [&](const Chunk &ch, f32x4 (&sa)[kCGd], f32x4 (&sb)[kCGd]) {
 #pragma unroll
@@ -383,17 +384,17 @@ decode_kernel(DecodeParams p) {
 #pragma unroll
             for (int i = 0; i < 8; ++i) s[i] = (sk >> i) & 1u ? s[i] : -INFINITY;
           }
-          const float lmax = max8(s);
-          if (__builtin_amdgcn_ballot_w64(lmax > m[cg] + thresh) != 0) {
+          const float lmax = max8(s) * c2;
+          if (__builtin_amdgcn_ballot_w64(lmax > m[cg] + kRescaleLog2) != 0) {
             const float cmax = max_xor32(max_xor16(lmax));
-            const bool up = cmax > m[cg] + thresh;
-            const float alpha = up ? fast_exp2((m[cg] - cmax) * c2) : 1.f;
+            const bool up = cmax > m[cg] + kRescaleLog2;
+            const float alpha = up ? fast_exp2(m[cg] - cmax) : 1.f;
             m[cg] = up ? cmax : m[cg];
             lsum[cg] *= alpha;
 #pragma unroll
             for (int dt = 0; dt < 8; ++dt) acc[cg][dt] *= alpha;
           }
-          const float mc = m[cg] * c2;
+          const float mc = m[cg];
           float pr[8];
 #pragma unroll
           for (int i = 0; i < 8; ++i) pr[i] = fast_exp2(fmaf(s[i], c2, -mc));
@@ -502,7 +503,7 @@ decode_kernel(DecodeParams p) {
           float wgt[kCoop<kSplit>], l = 0.f;
 #pragma unroll
           for (int w = 0; w < kCoop<kSplit>; ++w) {
-            wgt[w] = fast_exp2((s_m[w][cg][r] - mx) * c2);
+            wgt[w] = fast_exp2(s_m[w][cg][r] - mx);
             l += wgt[w] * s_l[w][cg][r];
           }
           // a column that sees no key at all (a query before position 0) writes zeros
@@ -542,7 +543,7 @@ decode_kernel(DecodeParams p) {
           float *dst = p.ws_o + (row[cg] * p.max_splits + piece) * kHeadDim + 4 * q;
 #pragma unroll
           for (int dt = 0; dt < 8; ++dt) *reinterpret_cast<f32x4 *>(dst + 16 * dt) = acc[cg][dt] * inv;
-          if (q == 0) p.ws_lse[row[cg] * p.max_splits + piece] = m[cg] * c2 + __log2f(l);
+          if (q == 0) p.ws_lse[row[cg] * p.max_splits + piece] = m[cg] + __log2f(l);
         }
       }
     }

@@ -326,7 +326,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
     }
   };
 
-  float m[kCG], lsum[kCG];
+  float m[kCG], lsum[kCG];  // m: running maximum in exp2 units
   f32x4 acc[kCG][8];
 #pragma unroll
   for (int cg = 0; cg < kCG; ++cg) {
@@ -428,16 +428,17 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   // and the tile's exponentials taken again. Otherwise every probability is
   // below 2^12 and m stays: the result is the same either way, because
   // numerator and denominator share m, and the 2^12 bound keeps both far
-  // inside the fp32 and bf16 ranges. The running maximum starts at -FLT_MAX, a
-  // finite value: exp2 of a masked score (-inf) is then 0 with no NaN from
-  // (-inf) - (-inf), and the first finite score always raises it (its
+  // inside the fp32 and bf16 ranges. The running maximum is kept in exp2
+  // units (score * scale * log2 e) and starts at -FLT_MAX, a finite value
+  // whatever the scale: exp2 of a masked score (-inf) is then 0 with no NaN
+  // from (-inf) - (-inf), and the first finite score always raises it (its
   // probability overflows to infinity; alpha = exp2(-huge) = 0).
   // The exponentials give the bf16 P^T operands; the row sums use the same
   // bf16-rounded probabilities as the PV product.
   auto tile_exp = [&](f32x4 (&sc)[2][2][kCG], u32x4 (&pf)[2][kCG], float (&ts)[kCG]) {
 #pragma unroll
     for (int cg = 0; cg < kCG; ++cg) {
-      const float mc = m[cg] * c2;
+      const float mc = m[cg];
       ts[cg] = 0.f;
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
@@ -466,9 +467,9 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
                              sc[0][1][cg][0], sc[0][1][cg][1], sc[0][1][cg][2], sc[0][1][cg][3]};
         const float b8[8] = {sc[1][0][cg][0], sc[1][0][cg][1], sc[1][0][cg][2], sc[1][0][cg][3],
                              sc[1][1][cg][0], sc[1][1][cg][1], sc[1][1][cg][2], sc[1][1][cg][3]};
-        const float cmax = max_xor32(max_xor16(max2(max8(a8), max8(b8))));
+        const float cmax = max_xor32(max_xor16(max2(max8(a8), max8(b8)))) * c2;
         const bool up = cmax > m[cg];
-        const float alpha = up ? fast_exp2((m[cg] - cmax) * c2) : 1.f;
+        const float alpha = up ? fast_exp2(m[cg] - cmax) : 1.f;
         m[cg] = up ? cmax : m[cg];
         lsum[cg] *= alpha;
 #pragma unroll

@@ -230,6 +230,19 @@ class Cache:
                       _ptr(self.block_table, "block_table", _i32()), self.stride)
 
 
+def _check_cache(shape: Shape, cache: Cache, ns: int):
+    """The pools and the table must match the shape the kernels are told."""
+    v = cache.v_pool.shape
+    if int(v[1]) != shape.num_kv_heads:
+        raise ValueError(f"pools hold {int(v[1])} KV heads, shape says {shape.num_kv_heads}")
+    if int(v[2]) * int(v[4]) != shape.page_size:
+        raise ValueError(f"pool page size {int(v[2]) * int(v[4])} != shape page size {shape.page_size}")
+    if int(v[3]) != shape.head_dim:
+        raise ValueError(f"pool head dim {int(v[3])} != shape head dim {shape.head_dim}")
+    if int(cache.block_table.shape[0]) < ns:
+        raise ValueError(f"block table has {int(cache.block_table.shape[0])} rows for {ns} sequences")
+
+
 def _stream(stream):
     import torch
 
@@ -295,6 +308,7 @@ def kv_append(layer: Layer, shape: Shape, cache: Cache, k_new, v_new, cu_seqlens
     args = (_ptr(k_new, "k_new", _bf16(), t * row), _ptr(v_new, "v_new", _bf16(), t * row),
             _ptr(cu_seqlens, "cu_seqlens", _i32(), ns + 1), _ptr(start_pos, "start_pos", _i32(), ns))
     slots = _ptr(slot_mapping_out, "slot_mapping_out", (torch.int64,), t) if slot_mapping_out is not None else None
+    _check_cache(shape, cache, ns)
     sh, ca = shape.c(), cache.c()
     st = load().hswa_kv_append(layer.c(), ctypes.byref(sh), ctypes.byref(ca), *args, ns, t, slots, _stream(stream))
     _check(st, "hswa_kv_append")
@@ -310,6 +324,7 @@ def prefill(layer: Layer, shape: Shape, cache: Cache, q, k_new, v_new, cu_seqlen
             _ptr(v_new, "v_new", _bf16(), t * krow), _ptr(cu_seqlens, "cu_seqlens", _i32(), ns + 1),
             _ptr(prefix_lens, "prefix_lens", _i32(), ns))
     o = _ptr(out, "out", _bf16(), t * qrow)
+    _check_cache(shape, cache, ns)
     sh, ca = shape.c(), cache.c()
     st = load().hswa_prefill(layer.c(), ctypes.byref(sh), ctypes.byref(ca), *args, ns, t, int(max_chunk_len), o,
                              _stream(stream))
@@ -340,6 +355,7 @@ def decode_multi(layer: Layer, shape: Shape, cache: Cache, q, context_lens, max_
     if workspace is not None:
         wp = _ptr(workspace, "workspace", (torch.uint8, torch.float32, torch.int32))
         wbytes = workspace.numel() * workspace.element_size()
+    _check_cache(shape, cache, ns)
     sh, ca = shape.c(), cache.c()
     st = load().hswa_decode_multi(layer.c(), ctypes.byref(sh), ctypes.byref(ca), qp, cp, ns, nq,
                                   int(max_context_len), wp, wbytes, o, _stream(stream))
@@ -360,6 +376,7 @@ def decode(layer: Layer, shape: Shape, cache: Cache, q, context_lens, max_contex
     if workspace is not None:
         wp = _ptr(workspace, "workspace", (torch.uint8, torch.float32, torch.int32))
         wbytes = workspace.numel() * workspace.element_size()
+    _check_cache(shape, cache, ns)
     sh, ca = shape.c(), cache.c()
     st = load().hswa_decode(layer.c(), ctypes.byref(sh), ctypes.byref(ca), qp, cp, ns, int(max_context_len), wp,
                             wbytes, o, _stream(stream))

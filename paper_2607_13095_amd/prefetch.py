@@ -85,13 +85,19 @@ class LayerwisePrefetch:
         n = len(plans)
         copied = [torch.cuda.Event() for _ in range(n)]
         done = [torch.cuda.Event() for _ in range(n)]
+        # work enqueued on the compute stream before this run (e.g. a previous
+        # run's attention, still reading the slots) finishes before any slot is
+        # overwritten
+        start = torch.cuda.Event()
+        start.record(comp)
 
         def issue_copy(l, stream):
             slot, prev = sched[l]
             dst = self.rings[kinds[l]][slot]
             with torch.cuda.stream(stream):
-                if prev >= 0 and stream is not comp:
-                    stream.wait_event(done[prev])  # the slot's previous user has finished
+                if stream is not comp:
+                    # the slot's previous user in this run, or anything before it
+                    stream.wait_event(done[prev] if prev >= 0 else start)
                 for d, h in zip(dst, plans[l].host):
                     d.copy_(h, non_blocking=True)
                 copied[l].record(stream)

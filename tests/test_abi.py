@@ -158,3 +158,61 @@ def test_workspace_and_split_len_host_helpers():
         else:
             assert wsb >= ns * 64 * splits * (128 + 1) * 4
     assert hswa.decode_split_len(hswa.Shape(64, 8, 64, 64), 4, 100) == -1
+
+
+def _decode_multi(layer, shape, cache, nq, ns=2, maxc=300):
+    lib = hswa.load()
+    return lib.hswa_decode_multi(layer, ctypes.byref(shape), ctypes.byref(cache), FAKE, FAKE, ns, nq, maxc, FAKE,
+                                 1 << 30, FAKE, None)
+
+
+def test_decode_multi_swa_query_limit():
+    """The first of nq new queries reads the W - 1 keys before it; a ring of R
+    pages keeps the latest R * PG positions, so an SWA ring layer accepts
+    nq <= R * PG - W + 1 and an explicit-release table (which stores the last
+    W positions of one extend) nq <= W. Beyond: HSWA_ERR_UNSUPPORTED before any
+    device work."""
+    sh16 = _shape(pg=16)
+    ring16 = OL.ring_pages(128, 16) * 16            # 144 positions held
+    assert ring16 - 128 + 1 == 17
+    assert _decode_multi(SWA128, sh16, _cache(stride=9), 18) == -2
+    assert _decode_multi(SWA128, sh16, _cache(stride=9), 64) == -2
+    assert _decode_multi(hswa._Layer(1, 5), sh16, _cache(stride=2), 29) == -2    # R = 2: 32 - 5 + 1 = 28
+    # SWA_PAGED: nq <= W
+    assert _decode_multi(hswa._Layer(2, 4), sh16, _cache(stride=32), 5) == -2
+    assert _decode_multi(hswa._Layer(2, 1), sh16, _cache(stride=32), 2) == -2
+    # the limits do not apply to FULL layers, nor at PG 64 / W 128 (65 > 64 queries)
+    assert _decode_multi(FULL, sh16, _cache(stride=32), 65) == -1    # 65 > 64: the general limit
+    for layer, cache, nq in ((SWA128, _cache(stride=3), 64), (hswa._Layer(2, 128), _cache(stride=8), 64)):
+        # legal counts pass validation; a null q then stops the call before any device work
+        lib = hswa.load()
+        sh = _shape()
+        st = lib.hswa_decode_multi(layer, ctypes.byref(sh), ctypes.byref(cache), None, FAKE, 2, nq, 300, FAKE,
+                                   1 << 30, FAKE, None)
+        assert st == -1
+    lib = hswa.load()
+    st = lib.hswa_decode_multi(SWA128, ctypes.byref(sh16), ctypes.byref(_cache(stride=9)), None, FAKE, 2, 17, 300,
+                               FAKE, 1 << 30, FAKE, None)
+    assert st == -1                                   # 17 is legal at PG 16: reaches the null-q check
+
+
+def test_binding_rejects_pools_that_disagree_with_the_shape():
+    """The binding checks pools and table against the shape before any call."""
+    import torch
+
+    sh = hswa.Shape(64, 8, 128, 64)
+
+    class T:  # stands in for device tensors: only .shape is read by the check
+        def __init__(self, *shape):
+            self.shape = torch.Size(shape)
+
+    def cache(hkv=8, pg=64, d=128, rows=4):
+        c = hswa.Cache.__new__(hswa.Cache)
+        c.v_pool = T(10, hkv, pg // min(pg, 32), d, min(pg, 32))
+        c.block_table = T(rows, 5)
+        return c
+
+    hswa._check_cache(sh, cache(), 4)
+    for bad, ns in ((cache(hkv=4), 4), (cache(pg=16), 4), (cache(d=64), 4), (cache(rows=3), 4)):
+        with pytest.raises(ValueError):
+            hswa._check_cache(sh, bad, ns)

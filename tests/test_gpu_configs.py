@@ -6,8 +6,7 @@ benchmark times, against the fp64 oracle.
   * decode_b64 (64 sequences, contexts 1K-32K, SWA + FULL): the benchmark's own
     step (append + decode of both layers); every output.
   * chunked_prefill_4x8k (4 x (8192 cached + 2048 new), SWA + FULL): the
-    benchmark's own prefill calls; 42 sampled query rows per sequence (tile
-    edges, the first and last rows, random rows), every head.
+    benchmark's own prefill calls; every output of both layers.
   * stack70 shapes (16 sequences at a 131072-token context): one FULL and one
     SWA layer at full size, sampled sequences; and the 70-layer stack (FULL iff
     layer % 7 == 6) at small contexts, every output of every layer.
@@ -21,6 +20,8 @@ a suffix of the history that still holds its whole window: attention is
 invariant under a shift of positions and keys outside the window have zero
 weight, so the result is the same as over the whole history.
 """
+
+import os
 
 import numpy as np
 import pytest
@@ -118,35 +119,54 @@ def test_cfg_decode_b64_bench_step(gpu_lib):
 # chunked_prefill_4x8k: the benchmark's own prefill calls
 # ---------------------------------------------------------------------------
 
+def _oracle_workers():
+    return max(1, min(16, len(os.sched_getaffinity(0))))
+
+
 def test_cfg_chunked_prefill_bench_calls(gpu_lib):
+    """Every output of both layers (4 x 2048 rows x 64 heads each) against the
+    oracle. The oracle runs once per (sequence, KV head) over that KV head's 8
+    query heads (the GQA group), the tasks spread over a thread pool with one
+    BLAS thread each; an SWA task sees the suffix of the history that holds
+    every window of its queries."""
     import bench
+    from concurrent.futures import ThreadPoolExecutor
+    from threadpoolctl import threadpool_limits
 
     wl = synth.chunked_prefill_4x8k()
     _say(f"[cfg] {wl.name}")
     pb = bench.PrefillBench(wl)
     P, C = np.asarray(wl.prefix), np.asarray(wl.new)
     cuP, cuC = synth.cu_seqlens(P), synth.cu_seqlens(C)
-    rng = synth.rng_of(wl.seed, 99)
+    G = wl.hq // wl.hkv
     for li, L in enumerate(pb.layers):
         pb.call(L)
         torch.cuda.synchronize()
         # the cached prefix was drawn with these seeds and appended at set-up
-        kp = synth.torch_normal_bf16((int(P.sum()), wl.hkv, D), "cuda", wl.seed, li, 0, synth.TAG_K)
-        vp = synth.torch_normal_bf16((int(P.sum()), wl.hkv, D), "cuda", wl.seed, li, 0, synth.TAG_V)
+        kp = _f64(synth.torch_normal_bf16((int(P.sum()), wl.hkv, D), "cuda", wl.seed, li, 0, synth.TAG_K))
+        vp = _f64(synth.torch_normal_bf16((int(P.sum()), wl.hkv, D), "cuda", wl.seed, li, 0, synth.TAG_V))
+        kn, vn, q, out = _f64(L["kn"]), _f64(L["vn"]), _f64(L["q"]), _f64(L["out"])
         w = wl.window if L["kind"] == "swa" else None
-        for b in range(wl.ns):
-            c = int(C[b])
-            rows = {0, 1, 31, 32, 63, 64, 255, 256, c - 2, c - 1}
-            rows |= {int(x) for x in rng.integers(0, c, 32)}
-            rows = np.array(sorted(r for r in rows if 0 <= r < c))
-            kh = np.concatenate([_f64(kp[cuP[b]:cuP[b + 1]]), _f64(L["kn"][cuC[b]:cuC[b + 1]])])
-            vh = np.concatenate([_f64(vp[cuP[b]:cuP[b + 1]]), _f64(L["vn"][cuC[b]:cuC[b + 1]])])
-            q = _f64(L["q"][cuC[b] + rows])
-            ref = OA.masked_attention(q, kh, vh, int(P[b]) + rows, w)
-            got = _f64(L["out"][cuC[b] + rows])
-            assert_close(got, ref, f"{wl.name} {L['kind']} seq {b}")
-        del kp, vp
-        torch.cuda.empty_cache()
+
+        def task(bg):
+            b, g = bg
+            p, c = int(P[b]), int(C[b])
+            kh = np.concatenate([kp[cuP[b]:cuP[b + 1], g:g + 1], kn[cuC[b]:cuC[b + 1], g:g + 1]])
+            vh = np.concatenate([vp[cuP[b]:cuP[b + 1], g:g + 1], vn[cuC[b]:cuC[b + 1], g:g + 1]])
+            lo = 0 if w is None else max(0, p - w + 1)  # the first query's window start
+            heads = slice(g * G, (g + 1) * G)
+            ref = OA.masked_attention(q[cuC[b]:cuC[b + 1], heads], kh[lo:], vh[lo:], np.arange(p, p + c) - lo, w)
+            assert_close(out[cuC[b]:cuC[b + 1], heads], ref, f"{wl.name} {L['kind']} seq {b} kv head {g}")
+            return b, g
+
+        tasks = [(b, g) for b in range(wl.ns) for g in range(wl.hkv)]
+        with threadpool_limits(1), ThreadPoolExecutor(_oracle_workers()) as ex:
+            done = list(ex.map(task, tasks))
+        assert len(done) == len(tasks)
+        _say(f"[cfg] {wl.name} {L['kind']}: all {int(C.sum())} rows x {wl.hq} heads checked")
+        del kp, vp, kn, vn, q, out
+    del pb
+    torch.cuda.empty_cache()
 
 
 # ---------------------------------------------------------------------------

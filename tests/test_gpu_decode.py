@@ -102,7 +102,7 @@ def test_decode_full_long(gpu_lib):
 def test_decode_context_clamp_and_empty(gpu_lib):
     """context_lens < 1 give zero rows; ns = 0 is a no-op."""
     shape = hswa.Shape(8, 1, 128, 16)
-    layer, kv = make_layer("full", 0, shape, [64], (205,))
+    layer, kv = make_layer("full", 0, shape, [64, 64], (205,))
     q = torch.zeros((2, 8, 128), dtype=torch.bfloat16, device="cuda")
     out = torch.full((2, 8, 128), 7.0, dtype=torch.bfloat16, device="cuda")
     hswa.decode(layer, shape, kv.cache, q, i32([0, -3]), 64, out)

@@ -18,11 +18,11 @@ pytestmark = pytest.mark.gpu
 D = 128
 
 
-def run_multi(kind, window, pg, hq, hkv, ctxs, nq, seed, ctx_override=None):
+def run_multi(kind, window, pg, hq, hkv, ctxs, nq, seed, ctx_override=None, scale=None):
     """ctxs: cached tokens before the nq new ones; returns (gpu, ref) [ns, nq, hq, D]."""
     ns = len(ctxs)
     final = [c + nq for c in ctxs]
-    shape = hswa.Shape(hq, hkv, D, pg)
+    shape = hswa.Shape(hq, hkv, D, pg, scale=scale)
     layer, kv = make_layer(kind, window, shape, final, seed)
     hist = SeqHistory(final, hkv, D, *seed)
     append_history(layer, shape, kv, hist, [0] * ns, ctxs)
@@ -43,7 +43,7 @@ def run_multi(kind, window, pg, hq, hkv, ctxs, nq, seed, ctx_override=None):
         ok = pos >= 0
         if ok.any():
             ref[b][ok] = OA.masked_attention(OA.bf16_bits_to_f64(qbits[b][ok]), OA.bf16_bits_to_f64(hist.k[b][:L]),
-                                             OA.bf16_bits_to_f64(hist.v[b][:L]), pos[ok], w)
+                                             OA.bf16_bits_to_f64(hist.v[b][:L]), pos[ok], w, shape.scale)
     return to_f64(out), ref, (layer, shape, kv, qbits, lens, maxc)
 
 
@@ -111,3 +111,34 @@ def test_decode_multi_short_context_zero_rows(gpu_lib):
     gpu, ref, _ = run_multi("full", 0, 16, 16, 2, [3, 3], 4, (904,), ctx_override=[2, 4])
     assert np.all(gpu[0][:2] == 0) and np.all(gpu[0][2:] != 0)
     assert_close(gpu, ref, "decode multi short")
+
+
+@pytest.mark.parametrize("pg,window,nq", [(16, 128, 17), (16, 5, 28), (64, 128, 64)])
+def test_decode_multi_swa_largest_legal_count(gpu_lib, pg, window, nq):
+    """The largest query count an SWA ring accepts, R * PG - W + 1 (capped at
+    64): the first query's window reaches back to the oldest position the ring
+    still holds once all nq tokens are appended. One more is rejected."""
+    print(f"[decode-multi-limit] pg={pg} W={window} nq={nq}", flush=True)
+    assert nq == min(64, hswa.ring_pages(window, pg) * pg - window + 1)
+    gpu, ref, (layer, shape, kv, qbits, lens, maxc) = run_multi("swa", window, pg, 16, 2, [0, 3, 150, 1000, 4097],
+                                                                nq, (906, pg, window))
+    assert_close(gpu, ref, f"decode multi SWA W={window} PG={pg} nq={nq}")
+    if nq < 64:
+        q = torch.zeros((5, nq + 1, 16, D), dtype=torch.bfloat16, device="cuda")
+        out = torch.empty_like(q)
+        with pytest.raises(hswa.HswaError) as e:
+            hswa.decode_multi(layer, shape, kv.cache, q, i32(lens), maxc, out)
+        assert e.value.status == -2
+
+
+@pytest.mark.parametrize("scale", [1.0, 4.0])
+@pytest.mark.parametrize("kind,window", [("full", 0), ("swa", 128), ("swa", 5)])
+def test_decode_multi_large_scale(gpu_lib, scale, kind, window):
+    """Scales above ln 2: columns whose wave sees none of their keys in a chunk
+    keep a finite running maximum (exp2 units) and give no NaN; single-query
+    decode too (nq = 1), on the one-pass and the split path."""
+    print(f"[decode-multi-scale] scale={scale} {kind} W={window}", flush=True)
+    ctxs = [0, 1, 63, 200, 3000, 9000]
+    for nq in (1, 4):
+        gpu, ref, _ = run_multi(kind, window, 64, 64, 8, ctxs, nq, (907, nq), scale=scale)
+        assert_close(gpu, ref, f"decode multi nq={nq} {kind} W={window} scale {scale}")

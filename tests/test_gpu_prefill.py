@@ -16,10 +16,10 @@ pytestmark = pytest.mark.gpu
 
 
 def run_prefill(kind, window, pg, hq, hkv, prefixes, chunks, seed, fill=float("nan"), perm_seed=None,
-                max_chunk=None):
+                max_chunk=None, scale=None):
     ns = len(prefixes)
     final = [p + c for p, c in zip(prefixes, chunks)]
-    shape = hswa.Shape(hq, hkv, 128, pg)
+    shape = hswa.Shape(hq, hkv, 128, pg, scale=scale)
     layer, kv = make_layer(kind, window, shape, final, perm_seed or seed, fill=fill)
     hist = SeqHistory(final, hkv, 128, *seed)
     append_history(layer, shape, kv, hist, [0] * ns, prefixes)
@@ -36,7 +36,8 @@ def run_prefill(kind, window, pg, hq, hkv, prefixes, chunks, seed, fill=float("n
     w = window if kind == "swa" else None
     refs, off = [], 0
     for b, (p, c) in enumerate(zip(prefixes, chunks)):
-        refs.append(OA.prefill(qf[off:off + c], OA.bf16_bits_to_f64(hist.k[b]), OA.bf16_bits_to_f64(hist.v[b]), p, w))
+        refs.append(OA.prefill(qf[off:off + c], OA.bf16_bits_to_f64(hist.k[b]), OA.bf16_bits_to_f64(hist.v[b]), p, w,
+                               shape.scale))
         off += c
     return gpu, np.concatenate(refs), (layer, shape, kv, hist, kn, vn)
 
@@ -73,3 +74,18 @@ def test_prefill_empty_chunks(gpu_lib):
     """Sequences with an empty chunk in the batch are skipped; max_chunk_len 0 is a no-op."""
     gpu, ref, _ = run_prefill("full", 0, 16, 8, 1, [5, 0, 40], [3, 0, 20], (303,))
     assert_close(gpu, ref, "empty chunk in batch")
+
+
+@pytest.mark.parametrize("scale", [1.0, 4.0])
+def test_prefill_large_scale(gpu_lib, scale):
+    """Scales above ln 2 (scale * log2 e > 1, e.g. queries that arrive
+    pre-scaled): the running maximum starts finite in exp2 units, so a column
+    whose first tile is wholly masked (SWA rows whose window starts past the
+    workgroup's first tile) gets no NaN. The 512-token SWA prefill (8 / 1 heads,
+    PG 16) and a chunk over a cached prefix at 64 / 8 heads, PG 64."""
+    print(f"[prefill-scale] scale={scale}", flush=True)
+    gpu, ref, _ = run_prefill("swa", 128, 16, 8, 1, [0], [512], (304, 1), scale=scale)
+    assert_close(gpu, ref, f"swa prefill 512, scale {scale}")
+    for kind, window in (("swa", 128), ("full", 0)):
+        gpu, ref, _ = run_prefill(kind, window, 64, 64, 8, [1000, 3], [2048, 700], (304, 2), scale=scale)
+        assert_close(gpu, ref, f"{kind} prefill over a prefix, scale {scale}")
