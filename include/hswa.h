@@ -237,6 +237,25 @@ hswa_status hswa_decode(hswa_layer layer, const hswa_shape *shape, const hswa_ca
                         int32_t max_context_len, void *workspace, size_t workspace_bytes,
                         void *out, void *stream);
 
+/* Bytes of the fixed device array behind hswa_decode_noalloc. */
+#define HSWA_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+
+/* hswa_decode for callers that cannot allocate device memory or hand in a
+ * workspace (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc): the same kernels and results, with the FULL split
+ * partials kept in a fixed device array of the library
+ * (HSWA_NOALLOC_SCRATCH_BYTES per device, taken on the first call on a device
+ * and held until the process ends). The call allocates nothing. A FULL layer
+ * whose partials need more (hswa_decode_workspace_bytes > the array) returns
+ * HSWA_ERR_CAPACITY; SWA layers use no scratch. Nothing in the array needs to
+ * start at zero: a call reads back only the partials it wrote. All calls on
+ * one device share the array and leave their partials in it: calls that
+ * overlap on one GPU (several streams, or threads) race and give wrong rows;
+ * serialise them, or use hswa_decode with a workspace of their own. */
+hswa_status hswa_decode_noalloc(hswa_layer layer, const hswa_shape *shape, const hswa_cache *cache,
+                                const void *q, const int32_t *context_lens, int32_t ns,
+                                int32_t max_context_len, void *out, void *stream);
+
 /* Multi-query decode ("MTP Optimization": the model verifies 1 + 3 predicted
  * tokens per sequence per step): num_queries (1 .. 64) new queries per
  * sequence at positions c_b - num_queries .. c_b - 1, where c_b =

@@ -225,9 +225,15 @@ int32_t hswa_decode_split_len(const hswa_shape *shape, int32_t ns, int32_t max_c
   return decode_geometry(shape, ns, max_context_len, 1).split_len;
 }
 
-hswa_status hswa_decode_multi(hswa_layer layer, const hswa_shape *shape, const hswa_cache *cache, const void *q,
-                              const int32_t *context_lens, int32_t ns, int32_t num_queries, int32_t max_context_len,
-                              void *workspace, size_t workspace_bytes, void *out, void *stream) {
+}  // extern "C"
+
+namespace {
+
+// Shared body of the decode entry points. With `noalloc` the FULL split
+// partials go to the library's fixed device array instead of `workspace`.
+hswa_status decode_impl(hswa_layer layer, const hswa_shape *shape, const hswa_cache *cache, const void *q,
+                        const int32_t *context_lens, int32_t ns, int32_t num_queries, int32_t max_context_len,
+                        void *workspace, size_t workspace_bytes, bool noalloc, void *out, void *stream) {
   hswa_status st;
   if ((st = check_layer(layer)) != HSWA_OK) return st;
   if ((st = check_shape(shape)) != HSWA_OK) return st;
@@ -258,8 +264,13 @@ hswa_status hswa_decode_multi(hswa_layer layer, const hswa_shape *shape, const h
     p.split_len = geo.split_len;
     p.max_splits = geo.max_splits;
     if (geo.max_splits > 1) {
-      if (!workspace) return HSWA_ERR_INVALID_ARG;
-      if (workspace_bytes < geo.total_bytes) return HSWA_ERR_CAPACITY;
+      if (noalloc) {
+        if (geo.total_bytes > HSWA_NOALLOC_SCRATCH_BYTES) return HSWA_ERR_CAPACITY;
+        if (hswa::noalloc_scratch(&workspace) != hipSuccess) return HSWA_ERR_LAUNCH;
+      } else {
+        if (!workspace) return HSWA_ERR_INVALID_ARG;
+        if (workspace_bytes < geo.total_bytes) return HSWA_ERR_CAPACITY;
+      }
       p.ws_o = static_cast<float *>(workspace);
       p.ws_lse = reinterpret_cast<float *>(static_cast<char *>(workspace) + geo.o_bytes);
     }
@@ -271,11 +282,28 @@ hswa_status hswa_decode_multi(hswa_layer layer, const hswa_shape *shape, const h
   return finish_launch(hswa::launch_decode(p, s), s);
 }
 
+}  // namespace
+
+extern "C" {
+
+hswa_status hswa_decode_multi(hswa_layer layer, const hswa_shape *shape, const hswa_cache *cache, const void *q,
+                              const int32_t *context_lens, int32_t ns, int32_t num_queries, int32_t max_context_len,
+                              void *workspace, size_t workspace_bytes, void *out, void *stream) {
+  return decode_impl(layer, shape, cache, q, context_lens, ns, num_queries, max_context_len, workspace,
+                     workspace_bytes, false, out, stream);
+}
+
 hswa_status hswa_decode(hswa_layer layer, const hswa_shape *shape, const hswa_cache *cache, const void *q,
                         const int32_t *context_lens, int32_t ns, int32_t max_context_len, void *workspace,
                         size_t workspace_bytes, void *out, void *stream) {
-  return hswa_decode_multi(layer, shape, cache, q, context_lens, ns, 1, max_context_len, workspace, workspace_bytes,
-                           out, stream);
+  return decode_impl(layer, shape, cache, q, context_lens, ns, 1, max_context_len, workspace, workspace_bytes, false,
+                     out, stream);
+}
+
+hswa_status hswa_decode_noalloc(hswa_layer layer, const hswa_shape *shape, const hswa_cache *cache, const void *q,
+                                const int32_t *context_lens, int32_t ns, int32_t max_context_len, void *out,
+                                void *stream) {
+  return decode_impl(layer, shape, cache, q, context_lens, ns, 1, max_context_len, nullptr, 0, true, out, stream);
 }
 
 const char *hswa_status_string(hswa_status status) {

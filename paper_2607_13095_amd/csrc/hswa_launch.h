@@ -72,6 +72,10 @@ hipError_t launch_kv_append(const AppendParams &p, hipStream_t stream);
 hipError_t launch_decode(const DecodeParams &p, hipStream_t stream);
 hipError_t launch_prefill(const PrefillParams &p, hipStream_t stream);
 
+// Device address of the library's fixed scratch array on the current device
+// (looked up once per device).
+hipError_t noalloc_scratch(void **ptr);
+
 // Fewest keys of a FULL decode wave's span; a multiple of 256.
 int32_t decode_split_len(int32_t ns, int32_t hkv, int32_t group, int32_t max_ctx);
 

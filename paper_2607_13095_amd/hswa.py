@@ -31,7 +31,11 @@ EXPORTS = ["hswa_ring_pages", "hswa_page_bytes", "hswa_build_block_table", "hswa
            "hswa_allocator_step_end", "hswa_allocator_free", "hswa_allocator_tables", "hswa_allocator_usage",
            "hswa_prefix_tree_create", "hswa_prefix_tree_destroy", "hswa_prefix_tree_insert",
            "hswa_prefix_tree_match", "hswa_prefix_tree_release_swa", "hswa_prefix_tree_evict",
-           "hswa_prefix_tree_stats", "hswa_decode_multi_workspace_bytes", "hswa_decode_multi"]
+           "hswa_prefix_tree_stats", "hswa_decode_multi_workspace_bytes", "hswa_decode_multi",
+           "hswa_decode_noalloc"]
+
+# bytes of the library's fixed device array behind hswa_decode_noalloc
+NOALLOC_SCRATCH_BYTES = 128 << 20
 
 
 class HswaError(RuntimeError):
@@ -90,6 +94,7 @@ def load():
         "hswa_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "hswa_decode_multi_workspace_bytes": (SZ, [SP, I32, I32, I32]),
         "hswa_decode_multi": (ctypes.c_int, [LP, SP, CP, P, P, I32, I32, I32, P, SZ, P, P]),
+        "hswa_decode_noalloc": (ctypes.c_int, [LP, SP, CP, P, P, I32, I32, P, P]),
         "hswa_allocator_create": (ctypes.c_int, [ctypes.POINTER(_AllocConfig), ctypes.POINTER(P)]),
         "hswa_allocator_destroy": (None, [P]),
         "hswa_allocator_admit": (ctypes.c_int, [P, I32, I64, I32]),
@@ -381,6 +386,22 @@ def decode(layer: Layer, shape: Shape, cache: Cache, q, context_lens, max_contex
     st = load().hswa_decode(layer.c(), ctypes.byref(sh), ctypes.byref(ca), qp, cp, ns, int(max_context_len), wp,
                             wbytes, o, _stream(stream))
     _check(st, "hswa_decode")
+
+
+def decode_noalloc(layer: Layer, shape: Shape, cache: Cache, q, context_lens, max_context_len: int, out,
+                   stream=None):
+    """Decode without a workspace (the library's fixed device array holds the
+    split partials); q, out [NS, Hq, D]; see hswa_decode_noalloc."""
+    ns = int(context_lens.numel())
+    qrow = shape.num_q_heads * shape.head_dim
+    qp = _ptr(q, "q", _bf16(), ns * qrow)
+    cp = _ptr(context_lens, "context_lens", _i32(), ns)
+    o = _ptr(out, "out", _bf16(), ns * qrow)
+    _check_cache(shape, cache, ns)
+    sh, ca = shape.c(), cache.c()
+    st = load().hswa_decode_noalloc(layer.c(), ctypes.byref(sh), ctypes.byref(ca), qp, cp, ns, int(max_context_len),
+                                    o, _stream(stream))
+    _check(st, "hswa_decode_noalloc")
 
 
 # ---------------------------------------------------------------------------

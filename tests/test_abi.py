@@ -216,3 +216,23 @@ def test_binding_rejects_pools_that_disagree_with_the_shape():
     for bad, ns in ((cache(hkv=4), 4), (cache(pg=16), 4), (cache(d=64), 4), (cache(rows=3), 4)):
         with pytest.raises(ValueError):
             hswa._check_cache(sh, bad, ns)
+
+
+def test_decode_noalloc_validation():
+    """The allocation-free decode validates like hswa_decode and rejects a FULL
+    call whose split partials exceed its fixed array, before any device work."""
+    lib = hswa.load()
+    sh = _shape()
+
+    def call(layer, cache, ns, maxc, q=FAKE):
+        return lib.hswa_decode_noalloc(layer, ctypes.byref(sh), ctypes.byref(cache), q, FAKE, ns, maxc, FAKE, None)
+
+    need = lib.hswa_decode_workspace_bytes(ctypes.byref(sh), 256, 65537)
+    assert need > hswa.NOALLOC_SCRATCH_BYTES
+    assert call(FULL, _cache(stride=1100), 256, 65537) == -3
+    fits = lib.hswa_decode_workspace_bytes(ctypes.byref(sh), 64, 32769)
+    assert 0 < fits <= hswa.NOALLOC_SCRATCH_BYTES
+    assert call(FULL, _cache(stride=600), 64, 32769, q=None) == -1    # fits: reaches the null-q check
+    assert call(FULL, _cache(stride=1), 2, 100) == -3                 # table too short, as hswa_decode
+    assert call(hswa._Layer(1, 0), _cache(), 2, 100) == -1            # SWA window < 1
+    assert call(SWA128, _cache(stride=3), 2, 100, q=None) == -1
