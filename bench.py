@@ -1,24 +1,30 @@
 """Benchmark of the hybrid-SWA paged attention hot path on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--no-prefill]
+                    [--roofline-only] [--copy-calibration]
 
-Workload (the decode configuration the headline metric is quoted on):
-  64 sequences, cached contexts uniform in [1024, 32768], one SWA layer
-  (W = 128) and one FULL layer, 64 query / 8 KV heads, head dim 128, bf16,
-  page size 64, pages placed by a seeded permutation. One step appends one new
-  token per sequence to both layers (hswa_kv_append) and decodes it
-  (hswa_decode): the whole decode hot path. Inputs are resident in HBM before
-  the timed region.
+Headline workload (the largest configuration that fits one GPU): a 70-layer
+hybrid decode step, 60 SWA layers (W = 128) and 10 FULL layers (FULL iff
+layer % 7 == 6), 16 sequences at a 131072-token cached context, 64 query / 8 KV
+heads, head dim 128, bf16, page size 64, pages placed by a seeded permutation.
+One step appends one new token per sequence to every layer (hswa_kv_append)
+and decodes it (hswa_decode). Every layer's pools hold their own synthetic KV
+(86 GB of FULL pages, 12 MiB per SWA layer), resident in HBM before the timed
+region. value = algorithmic decode bytes of the step (K and V of every visible
+key read once per (sequence, KV head, layer), plus q and o) / step time.
 
-Also measured (same run, reported under "prefill"): chunked prefill of 4
-sequences with an 8192-token cached prefix and a 2048-token chunk, one SWA and
-one FULL layer (hswa_prefill then hswa_kv_append).
+The roofline entry is the FULL-layer decode call of that step (split-KV kernel
++ log-sum-exp merge), timed back to back with HIP events on the stream it runs
+on. Per-call timings elsewhere are medians with p10 / p90 over calls each
+preceded (outside the events) by a 1 GiB device write that evicts the
+memory-side cache.
 
-value = algorithmic decode bytes (K and V of every visible key read once per
-(sequence, KV head, layer), plus q and o) / step time. The roofline entry is
-for the FULL-layer decode call (split-KV kernel + log-sum-exp merge), timed with
-HIP events on the stream it runs on, inside the timed region.
-The CPU baseline is the fp64 oracle on a bounded sample of the same workload.
+Also measured in the same run: the 64-sequence decode (contexts 1K-32K), the
+512-token SWA prefill (8 / 1 heads, page size 16), chunked prefill (4 x (8192
+cached + 2048 new), timed calls are hswa_prefill alone), layerwise prefetch,
+multi-query decode, the explicit-release allocator, the window-safe prefix
+tree and the mixed prefill + decode step. The CPU baselines time the fp64
+oracle on bounded samples of the same workloads on the host's cores.
 """
 
 from __future__ import annotations
@@ -37,20 +43,22 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2516.6
+FLUSH_BYTES = 1 << 30  # a write this large evicts the 256 MB memory-side cache
 
 # Bytes moved between L2 and memory per call, from rocprofv3 --pmc FETCH_SIZE and
-# --pmc WRITE_SIZE runs of this script with --copy-calibration, each counter
-# scaled by what it reads for the plain 1 GiB copy (FETCH_SIZE reads 524,300 KiB
-# for 1 GiB read: x2.0; WRITE_SIZE reads 1,048,576 KiB for 1 GiB written: x1.0).
-# A figure holds only for the kernel sources it was taken on (SHA-256 below);
-# once they change the benchmark reports null until it is measured again.
+# --pmc WRITE_SIZE runs of this script with --roofline-only --copy-calibration,
+# each counter scaled by what it reads for the plain 1 GiB copy (FETCH_SIZE
+# reads 524,300 KiB for 1 GiB read: x2.0; WRITE_SIZE reads 1,048,576 KiB for
+# 1 GiB written: x1.0). A figure holds only for the kernel sources it was taken
+# on (SHA-256 below); once they change the benchmark reports null until it is
+# measured again.
 MEASURED_TRAFFIC = {
-    "decode_full": {"sources": ["decode.hip", "hswa_common.h", "hswa_launch.h"],
-                    "sha256": "a3f66ed9d3e531aac9d80aa9c69110a213dbcd93cc88299e96a6bacde1a87893",
-                    "fetch_bytes": 4100957394, "write_bytes": 34749121},
+    "decode_full_stack70": {"sources": ["decode.hip", "hswa_common.h", "hswa_launch.h"],
+                            "sha256": "",
+                            "fetch_bytes": 0, "write_bytes": 0},
     "prefill_full": {"sources": ["prefill.hip", "hswa_common.h", "hswa_launch.h"],
-                     "sha256": "0f480bc1173720a12440ca104f61931cab2c2ffbe7cd6fb8b16772aa08ca3a76",
-                     "fetch_bytes": 453118809, "write_bytes": 134217728},
+                     "sha256": "",
+                     "fetch_bytes": 0, "write_bytes": 0},
 }
 
 
@@ -67,7 +75,7 @@ def sources_sha256(names):
 def measured_traffic(key):
     """HBM-side bytes per call of a kernel, or None if its sources changed."""
     t = MEASURED_TRAFFIC[key]
-    if sources_sha256(t["sources"]) != t["sha256"]:
+    if not t["sha256"] or sources_sha256(t["sources"]) != t["sha256"]:
         return None
     return int(t["fetch_bytes"] + t["write_bytes"])
 
@@ -79,13 +87,13 @@ def log(*a):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prefill", action="store_true")
     ap.add_argument("--roofline-only", action="store_true",
-                    help="only the decode step and the prefill calls the roofline entries time (for counter runs)")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target oracle time for the CPU baseline")
+                    help="only the headline step and the prefill calls the roofline entries time (for counter runs)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target oracle time of the headline CPU baseline")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 1 GiB device copy three times (reference for HBM byte counters)")
     return ap.parse_args()
@@ -111,7 +119,272 @@ def copy_calibration():
 
 
 # ----------------------------------------------------------------------------
-# decode workload
+# timing helpers
+# ----------------------------------------------------------------------------
+
+class MallFlush:
+    """Writes FLUSH_BYTES of device memory (a fill kernel) so that the next
+    call starts with nothing of its inputs in the memory-side cache."""
+
+    def __init__(self):
+        import torch
+
+        self.buf = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device="cuda")
+        self.k = 0
+
+    def __call__(self):
+        self.k += 1
+        self.buf.fill_(float(self.k))
+
+
+def time_calls(fn, flush, reps=20, warmup=3):
+    """Per-call event timing: median, p10 and p90 (ms) over `reps` calls, each
+    preceded by a memory-side cache flush outside the events."""
+    import torch
+
+    for _ in range(warmup):
+        fn()
+    ts = []
+    for _ in range(reps):
+        flush()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        fn()
+        b.record()
+        b.synchronize()
+        ts.append(a.elapsed_time(b))
+    ts = np.asarray(ts)
+    return {"ms_median": round(float(np.median(ts)), 5), "ms_p10": round(float(np.percentile(ts, 10)), 5),
+            "ms_p90": round(float(np.percentile(ts, 90)), 5), "reps": reps, "mall_flushed": True}
+
+
+def time_back_to_back(fn, reps, warmup=2):
+    """Mean time (ms) of `reps` calls issued back to back between one pair of
+    HIP events on the current stream (no host gap per call)."""
+    import torch
+
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        fn()
+    b.record()
+    b.synchronize()
+    return a.elapsed_time(b) / reps
+
+
+def rate(nbytes=None, flops=None, ms=None):
+    out = {}
+    if nbytes is not None:
+        gbs = nbytes / (ms * 1e-3) / 1e9
+        out.update(gbs=round(gbs, 1), frac_hbm=round(gbs / HBM_PEAK_GBS, 4))
+    if flops is not None:
+        tf = flops / (ms * 1e-3) / 1e12
+        out.update(tflops=round(tf, 2), frac_mfma=round(tf / MFMA_BF16_PEAK_TFLOPS, 4))
+    return out
+
+
+# ----------------------------------------------------------------------------
+# CPU description
+# ----------------------------------------------------------------------------
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _blas_info():
+    try:
+        from threadpoolctl import threadpool_info
+
+        return [{"library": i.get("internal_api"), "version": i.get("version"), "threads": i.get("num_threads")}
+                for i in threadpool_info() if i.get("user_api") == "blas"]
+    except Exception:
+        return []
+
+
+def _blas_threads():
+    info = _blas_info()
+    return int(max((i["threads"] or 1 for i in info), default=1))
+
+
+def _host_cores():
+    return len(os.sched_getaffinity(0))
+
+
+def _host_f64(t):
+    import torch
+
+    from oracle import attention as OA
+
+    return OA.bf16_bits_to_f64(t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16))
+
+
+# ----------------------------------------------------------------------------
+# headline: the 70-layer hybrid decode step
+# ----------------------------------------------------------------------------
+
+class Stack70Bench:
+    """The 70-layer hybrid decode step (10 FULL + 60 SWA layers, 16 sequences
+    at a 131072-token context): every layer's pools hold their own synthetic KV
+    and one step appends the new token and decodes it in every layer."""
+
+    def __init__(self):
+        import torch
+
+        import synth
+        from paper_2607_13095_amd import hswa
+        from paper_2607_13095_amd.kvcache import LayerKV, pages_for
+
+        self.wl = wl = synth.stack70_decode()
+        dev = "cuda"
+        hq, hkv, d, pg, W = wl.hq, wl.hkv, wl.head_dim, wl.page_size, wl.window
+        ns = wl.ns
+        self.ctx = ctx = np.asarray(wl.prefix, dtype=np.int64)
+        final = (ctx + 1).tolist()
+        self.maxc = int(max(final))
+        self.shape = shape = hswa.Shape(hq, hkv, d, pg)
+        i32 = lambda x: torch.as_tensor(np.asarray(x, dtype=np.int32), device=dev)  # noqa: E731
+        self.ring = ring = hswa.ring_pages(W, pg)
+        self.ws = torch.empty(max(1, hswa.decode_workspace_bytes(shape, ns, self.maxc)), dtype=torch.uint8,
+                              device=dev)
+        self.layers = []
+        for li, kind in enumerate(wl.layers):
+            layer = hswa.Layer.swa(W) if kind == "swa" else hswa.Layer.full()
+            kv = LayerKV(layer, shape, final, perm=synth.page_permutation(pages_for(layer, pg, final), wl.seed, li))
+            # cached history: every position for FULL (four sequences at a time),
+            # the positions the ring keeps for SWA
+            first = self.first_cached(kind)
+            for b0 in range(0, ns, 4):
+                sl = slice(b0, min(ns, b0 + 4))
+                kh, vh, lens = self.history(li, kind, b0)
+                sub = hswa.Cache(kv.k_pool, kv.v_pool, kv.block_table[sl])
+                hswa.kv_append(layer, shape, sub, kh, vh, i32(synth.cu_seqlens(lens)), i32(first[sl]))
+                del kh, vh
+            self.layers.append(dict(
+                li=li, kind=kind, layer=layer, kv=kv,
+                k_new=synth.torch_normal_bf16((ns, hkv, d), dev, wl.seed, li, 0, synth.TAG_KDEC),
+                v_new=synth.torch_normal_bf16((ns, hkv, d), dev, wl.seed, li, 0, synth.TAG_VDEC),
+                q=synth.torch_normal_bf16((ns, hq, d), dev, wl.seed, li, 0, synth.TAG_QDEC),
+                out=torch.empty((ns, hq, d), dtype=torch.bfloat16, device=dev)))
+        torch.cuda.synchronize()
+        self.cu1, self.start, self.lens = i32(np.arange(ns + 1)), i32(ctx), i32(final)
+        row, qo = hkv * d * 2 * 2, 2 * ns * hq * d * 2
+        self.nfull = sum(1 for L in self.layers if L["kind"] == "full")
+        self.nswa = len(self.layers) - self.nfull
+        self.full_layer_bytes = int(np.sum(ctx + 1)) * row + qo
+        self.swa_layer_bytes = int(np.sum(np.minimum(W, ctx + 1))) * row + qo
+        self.bytes = self.nfull * self.full_layer_bytes + self.nswa * self.swa_layer_bytes
+        page_b = hswa.page_bytes(shape)
+        self.pool_bytes = {"full_layer": 2 * pages_for(hswa.Layer.full(), pg, final) * page_b,
+                           "swa_layer": 2 * pages_for(hswa.Layer.swa(W), pg, final) * page_b}
+
+    def first_cached(self, kind):
+        if kind == "full":
+            return np.zeros(self.wl.ns, dtype=np.int64)
+        return np.maximum(0, self.ctx - self.ring * self.wl.page_size)
+
+    def history(self, li, kind, b0):
+        """The seeded cached K / V of sequences b0 .. b0+3 of layer li (device)."""
+        import synth
+
+        wl = self.wl
+        first = self.first_cached(kind)
+        sl = slice(b0, min(wl.ns, b0 + 4))
+        lens = self.ctx[sl] - first[sl]
+        T = int(lens.sum())
+        kh = synth.torch_normal_bf16((T, wl.hkv, wl.head_dim), "cuda", wl.seed, li, b0, synth.TAG_K)
+        vh = synth.torch_normal_bf16((T, wl.hkv, wl.head_dim), "cuda", wl.seed, li, b0, synth.TAG_V)
+        return kh, vh, lens
+
+    def append(self, L):
+        from paper_2607_13095_amd import hswa
+
+        hswa.kv_append(L["layer"], self.shape, L["kv"].cache, L["k_new"], L["v_new"], self.cu1, self.start)
+
+    def decode(self, L):
+        from paper_2607_13095_amd import hswa
+
+        hswa.decode(L["layer"], self.shape, L["kv"].cache, L["q"], self.lens, self.maxc, L["out"], workspace=self.ws)
+
+    def run(self, kinds=("full", "swa")):
+        for L in self.layers:
+            if L["kind"] in kinds:
+                self.append(L)
+                self.decode(L)
+
+    def graph(self, kinds):
+        """The step (or one kind's layers) captured as one HIP graph."""
+        import torch
+
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            self.run(kinds)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g):
+            self.run(kinds)
+        return g
+
+    def cpu_baseline(self, target_s):
+        """fp64 oracle on the host cores over a sample of the step: every
+        sequence of SWA layer 0, then the sequences of the FULL layers in order
+        until about target_s seconds of oracle time. Inputs are regenerated on
+        the GPU from their seeds and copied to the host (untimed)."""
+        from oracle import attention as OA
+
+        wl = self.wl
+        W = wl.window
+        done_bytes, t_total, pairs = 0, 0.0, []
+        row, qo = wl.hkv * wl.head_dim * 2 * 2, 2 * wl.hq * wl.head_dim * 2
+        order = [L for L in self.layers if L["kind"] == "swa"][:1] + [L for L in self.layers if L["kind"] == "full"]
+        for L in order:
+            window = W if L["kind"] == "swa" else None
+            first = self.first_cached(L["kind"])
+            for b0 in range(0, wl.ns, 4):
+                kh, vh, lens = self.history(L["li"], L["kind"], b0)
+                cu = np.concatenate([[0], np.cumsum(lens)])
+                for i in range(len(lens)):
+                    b = b0 + i
+                    c = int(self.ctx[b])
+                    lo = 0 if window is None else max(0, c + 1 - window) - int(first[b])
+                    k = np.concatenate([_host_f64(kh[int(cu[i]) + lo:int(cu[i + 1])]), _host_f64(L["k_new"][b:b + 1])])
+                    v = np.concatenate([_host_f64(vh[int(cu[i]) + lo:int(cu[i + 1])]), _host_f64(L["v_new"][b:b + 1])])
+                    q = _host_f64(L["q"][b])
+                    t0 = time.perf_counter()
+                    OA.decode(q, k, v, window, self.shape.scale)
+                    t_total += time.perf_counter() - t0
+                    done_bytes += k.shape[0] * row + qo
+                    pairs.append((L["li"], b))
+                    del k, v
+                    if L["kind"] == "full" and t_total >= target_s:
+                        break
+                del kh, vh
+                if L["kind"] == "full" and t_total >= target_s:
+                    break
+            if t_total >= target_s:
+                break
+        nfull = sum(1 for li, _ in pairs if self.layers[li]["kind"] == "full")
+        return {"value": round(done_bytes / t_total / 1e9, 4), "unit": "GB/s", "cores": _blas_threads(),
+                "kind": "oracle", "cpu_model": _cpu_model(), "host_cores": _host_cores(), "blas": _blas_info(),
+                "sample": f"stack70 decode: the 16 sequences of SWA layer 0 and {nfull} (FULL layer, sequence) "
+                          f"decodes at a 131073-token context, each an fp64 numpy oracle call over the "
+                          f"sequence's contiguous history (inputs regenerated from their seeds, untimed); "
+                          f"{t_total:.1f} s of oracle time, {done_bytes / 1e9:.2f} GB of algorithmic bytes"}
+
+
+# ----------------------------------------------------------------------------
+# decode_b64 (64 sequences, contexts uniform in [1024, 32768])
 # ----------------------------------------------------------------------------
 
 class DecodeBench:
@@ -180,103 +453,41 @@ class DecodeBench:
         fn = hswa.decode if self.nq == 1 else hswa.decode_multi
         fn(L["layer"], self.shape, L["kv"].cache, L["q"], self.ctx_lens, self.maxc, L["out"], workspace=L["ws"])
 
-    def time_kind_back_to_back(self, kind, reps):
-        """Mean time of one layer kind's decode call over reps calls issued back
-        to back between one pair of HIP events on the current stream."""
-        import torch
-
-        L = next(x for x in self.layers if x["kind"] == kind)
-        self.decode(L)
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        a.record()
-        for _ in range(reps):
-            self.decode(L)
-        b.record()
-        b.synchronize()
-        return a.elapsed_time(b) / reps
-
-    def time_kind(self, kind, reps=20):
-        """Event timing of one layer kind's decode call alone (median of reps)."""
-        import torch
-
-        L = next(x for x in self.layers if x["kind"] == kind)
-        ts = []
-        for _ in range(reps):
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record()
-            self.decode(L)
-            b.record()
-            b.synchronize()
-            ts.append(a.elapsed_time(b))
-        return float(np.median(ts))
+    def kind(self, kind):
+        return next(x for x in self.layers if x["kind"] == kind)
 
     def cpu_baseline(self, target_s):
-        """fp64 oracle over the sequences (both layers) until ~target_s seconds of
-        oracle time. When a whole pass would take less, each oracle call is
-        repeated (the count estimated from the first sequence's share of the
-        keys), so the rate is measured over about target_s seconds."""
-        import math
-
+        """fp64 oracle over the sequences (both layers), in order, until about
+        target_s seconds of oracle time."""
         from oracle import attention as OA
 
-        threads = _blas_threads()
-        done_bytes, t_total, nseq, reps = 0, 0.0, 0, 1
+        done_bytes, t_total, nseq = 0, 0.0, 0
         row = self.wl.hkv * self.wl.head_dim * 2 * 2
         qo = 2 * self.wl.hq * self.wl.head_dim * 2
         W = self.wl.window
-
-        def keys(c):  # keys both layers read for a sequence with c cached tokens
-            return sum(c + 1 if L["kind"] == "full" else min(W, c + 1) for L in self.layers)
-
         for b in range(self.wl.ns):
             for L in self.layers:
                 c = int(self.ctx[b])
                 lo = int(L["cu"][b])
                 window = W if L["kind"] == "swa" else None
                 first = 0 if window is None else max(0, c + 1 - window)
-                # host copies of exactly the inputs the GPU read (untimed)
-                k = _host_f64(L["k_hist"][lo + first:lo + c])
-                v = _host_f64(L["v_hist"][lo + first:lo + c])
-                k = np.concatenate([k, _host_f64(L["k_new"][b:b + 1])])
-                v = np.concatenate([v, _host_f64(L["v_new"][b:b + 1])])
+                k = np.concatenate([_host_f64(L["k_hist"][lo + first:lo + c]), _host_f64(L["k_new"][b:b + 1])])
+                v = np.concatenate([_host_f64(L["v_hist"][lo + first:lo + c]), _host_f64(L["v_new"][b:b + 1])])
                 q = _host_f64(L["q"][b])
-                for _ in range(reps):
-                    t0 = time.perf_counter()
-                    OA.decode(q, k, v, window, self.shape.scale)
-                    t_total += time.perf_counter() - t0
-                    done_bytes += k.shape[0] * row + qo
+                t0 = time.perf_counter()
+                OA.decode(q, k, v, window, self.shape.scale)
+                t_total += time.perf_counter() - t0
+                done_bytes += k.shape[0] * row + qo
             nseq += 1
-            if b == 0:
-                est_pass = t_total * sum(keys(int(c)) for c in self.ctx) / keys(int(self.ctx[0]))
-                reps = max(1, min(20, math.ceil(target_s / est_pass)))
             if t_total >= target_s:
                 break
-        return {"value": done_bytes / t_total / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
-                "sample": f"first {nseq} of {self.wl.ns} sequences, both layers, each oracle call after the "
-                          f"first sequence's repeated {reps}x, fp64 numpy oracle, {t_total:.1f} s of oracle time"}
-
-
-def _host_f64(t):
-    import torch
-
-    from oracle import attention as OA
-
-    return OA.bf16_bits_to_f64(t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16))
-
-
-def _blas_threads():
-    try:
-        from threadpoolctl import threadpool_info
-
-        info = threadpool_info()
-        return int(max((i.get("num_threads", 1) for i in info if i.get("user_api") == "blas"), default=1))
-    except Exception:
-        return 1
+        return {"value": round(done_bytes / t_total / 1e9, 4), "unit": "GB/s", "cores": _blas_threads(),
+                "kind": "oracle", "sample": f"first {nseq} of {self.wl.ns} sequences, both layers, one fp64 "
+                                            f"oracle call each, {t_total:.1f} s of oracle time"}
 
 
 # ----------------------------------------------------------------------------
-# prefill workload
+# chunked prefill (4 x (8192 cached + 2048 new))
 # ----------------------------------------------------------------------------
 
 class PrefillBench:
@@ -314,21 +525,24 @@ class PrefillBench:
             kn = synth.torch_normal_bf16((T, hkv, d), dev, wl.seed, li, 1, synth.TAG_K)
             vn = synth.torch_normal_bf16((T, hkv, d), dev, wl.seed, li, 1, synth.TAG_V)
             out = torch.empty((T, hq, d), dtype=torch.bfloat16, device=dev)
-            self.layers.append(dict(kind=kind, layer=layer, kv=kv, q=q, kn=kn, vn=vn, out=out))
+            self.layers.append(dict(li=li, kind=kind, layer=layer, kv=kv, q=q, kn=kn, vn=vn, out=out))
         torch.cuda.synchronize()
         self.flops, self.bytes = {}, {}
         for L in self.layers:
-            pairs = 0
-            for p, c in zip(P, C):
-                if L["kind"] == "full":
-                    pairs += int(c * p + c * (c + 1) // 2)
-                else:
-                    pos = np.arange(p, p + c)
-                    pairs += int(np.minimum(W, pos + 1).sum())
-            self.flops[L["kind"]] = 4 * d * hq * pairs
+            self.flops[L["kind"]] = 4 * d * hq * self.pairs(L["kind"])
             keys = int((P + C).sum()) if L["kind"] == "full" else int(
                 sum(min(int(p), W - 1) + int(c) for p, c in zip(P, C)))
             self.bytes[L["kind"]] = keys * hkv * d * 4 + 2 * T * hq * d * 2
+
+    def pairs(self, kind, rows=None):
+        """Allowed (query, key) pairs of a layer kind; `rows` restricts each
+        sequence to the chunk rows it lists."""
+        W = self.wl.window
+        total = 0
+        for p, c in zip(self.P, self.C):
+            pos = p + (np.arange(c) if rows is None else np.asarray(rows))
+            total += int((pos + 1).sum()) if kind == "full" else int(np.minimum(W, pos + 1).sum())
+        return total
 
     def call(self, L):
         from paper_2607_13095_amd import hswa
@@ -336,29 +550,132 @@ class PrefillBench:
         hswa.prefill(L["layer"], self.shape, L["kv"].cache, L["q"], L["kn"], L["vn"], self.cu, self.pre, self.maxc,
                      L["out"])
 
-    def time_kind(self, kind, reps=20, warmup=10):
-        import torch
+    def kind(self, kind):
+        return next(x for x in self.layers if x["kind"] == kind)
 
-        L = next(x for x in self.layers if x["kind"] == kind)
-        for _ in range(warmup):
-            self.call(L)
+    def cpu_baseline(self, full_rows=512, workers=None):
+        """fp64 oracle rates on the host cores, one task per (sequence, KV head)
+        (the oracle over that KV head's query heads), the tasks spread over a
+        thread pool of `workers` with one BLAS thread each. SWA: the whole layer
+        (each task sees the suffix of the history that holds its windows).
+        FULL: the last `full_rows` rows of every chunk (the longest ones) of
+        half of the tasks, then extrapolated by algorithmic flops."""
+        from concurrent.futures import ThreadPoolExecutor
+
+        import synth
+        from oracle import attention as OA
+        from threadpoolctl import threadpool_limits
+
+        wl = self.wl
+        workers = workers or max(1, min(16, _host_cores()))
+        G, W = wl.hq // wl.hkv, wl.window
+        cuP, cuC = synth.cu_seqlens(self.P), synth.cu_seqlens(self.C)
+        res = {}
+        for L in self.layers:
+            kind = L["kind"]
+            kp = _host_f64(synth.torch_normal_bf16((int(self.P.sum()), wl.hkv, wl.head_dim), "cuda", wl.seed,
+                                                   L["li"], 0, synth.TAG_K))
+            vp = _host_f64(synth.torch_normal_bf16((int(self.P.sum()), wl.hkv, wl.head_dim), "cuda", wl.seed,
+                                                   L["li"], 0, synth.TAG_V))
+            kn, vn, q = _host_f64(L["kn"]), _host_f64(L["vn"]), _host_f64(L["q"])
+            rows = None if kind == "swa" else np.arange(int(self.C.min()) - full_rows, int(self.C.min()))
+            tasks = [(b, g) for b in range(wl.ns) for g in range(wl.hkv)]
+            if kind == "full":
+                tasks = tasks[: len(tasks) // 2]
+            inputs = []
+            for b, g in tasks:
+                p, c = int(self.P[b]), int(self.C[b])
+                kh = np.concatenate([kp[cuP[b]:cuP[b + 1], g:g + 1], kn[cuC[b]:cuC[b + 1], g:g + 1]])
+                vh = np.concatenate([vp[cuP[b]:cuP[b + 1], g:g + 1], vn[cuC[b]:cuC[b + 1], g:g + 1]])
+                r = np.arange(c) if rows is None else rows
+                lo = 0 if kind == "full" else max(0, p + int(r[0]) - W + 1)
+                inputs.append((q[cuC[b] + r, g * G:(g + 1) * G], kh[lo:], vh[lo:], p + r - lo))
+            window = W if kind == "swa" else None
+            with threadpool_limits(1), ThreadPoolExecutor(workers) as ex:
+                t0 = time.perf_counter()
+                list(ex.map(lambda a: OA.masked_attention(a[0], a[1], a[2], a[3], window, self.shape.scale), inputs))
+                dt = time.perf_counter() - t0
+            frac_tasks = len(tasks) / (wl.ns * wl.hkv)
+            flops = 4 * wl.head_dim * wl.hq * self.pairs(kind, rows) * frac_tasks
+            entry = {"gflops": round(flops / dt / 1e9, 3), "seconds": round(dt, 2), "threads": workers}
+            if kind == "swa":
+                entry.update(gbs=round(self.bytes["swa"] / dt / 1e9, 4), sample="whole layer (measured)")
+            else:
+                entry.update(extrapolated_layer_seconds=round(dt * self.flops["full"] / flops, 1),
+                             sample=f"{len(tasks)} of {wl.ns * wl.hkv} (sequence, KV head) tasks, the last "
+                                    f"{full_rows} rows of each chunk; whole-layer time extrapolated by flops")
+            res[kind] = entry
+            del kp, vp, kn, vn, q, inputs
+        return {"kind": "oracle", "unit": "GFLOP/s", "cores": workers, **res}
+
+
+# ----------------------------------------------------------------------------
+# swa_prefill_512 (one SWA layer, no cache, 8 / 1 heads, page size 16)
+# ----------------------------------------------------------------------------
+
+def swa512_report(flush, cpu=True):
+    """The 512-token SWA prefill (then its append) of one 8 / 1-head layer over
+    a ring of 9 pages of 16 tokens: a few microseconds of work, so its time is
+    launch latency; reported for completeness."""
+    import torch
+
+    import synth
+    from paper_2607_13095_amd import hswa
+    from paper_2607_13095_amd.kvcache import LayerKV, pages_for
+
+    wl = synth.swa_prefill_512()
+    C, W, pg, d = wl.new[0], wl.window, wl.page_size, wl.head_dim
+    shape = hswa.Shape(wl.hq, wl.hkv, d, pg)
+    layer = hswa.Layer.swa(W)
+    kv = LayerKV(layer, shape, [C], perm=synth.page_permutation(pages_for(layer, pg, [C]), wl.seed, 0))
+    qb = synth.normal_bf16((C, wl.hq, d), wl.seed, 0, 0, synth.TAG_Q)
+    kb = synth.normal_bf16((C, wl.hkv, d), wl.seed, 0, 0, synth.TAG_K)
+    vb = synth.normal_bf16((C, wl.hkv, d), wl.seed, 0, 0, synth.TAG_V)
+    dev = lambda x: torch.from_numpy(x.view(np.int16)).view(torch.bfloat16).cuda()  # noqa: E731
+    q, k, v = dev(qb), dev(kb), dev(vb)
+    out = torch.empty((C, wl.hq, d), dtype=torch.bfloat16, device="cuda")
+    cu, pre = (torch.tensor(x, dtype=torch.int32, device="cuda") for x in ([0, C], [0]))
+
+    def prefill():
+        hswa.prefill(layer, shape, kv.cache, q, k, v, cu, pre, C, out)
+
+    def step():
+        prefill()
+        hswa.kv_append(layer, shape, kv.cache, k, v, cu, pre)
+
+    pos = np.arange(C)
+    pairs = int(np.minimum(W, pos + 1).sum())
+    flops = 4 * d * wl.hq * pairs
+    nbytes = 2 * C * wl.hq * d * 2 + 2 * C * wl.hkv * d * 2
+    t = time_calls(prefill, flush)
+    b2b = time_back_to_back(prefill, 50)
+    rep = {"workload": wl.name, "prefill": t, "prefill_back_to_back_ms": round(b2b, 5),
+           "prefill_and_append": time_calls(step, flush), "algorithmic_flops": flops, "algorithmic_bytes": nbytes,
+           **rate(nbytes, flops, b2b), "note": "microseconds of work: bound by launch latency"}
+    if cpu:
+        from oracle import attention as OA
+
+        qf, kf, vf = (OA.bf16_bits_to_f64(x) for x in (qb, kb, vb))
         ts = []
-        for _ in range(reps):
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record()
-            self.call(L)
-            b.record()
-            b.synchronize()
-            ts.append(a.elapsed_time(b))
-        return float(np.median(ts))
+        for _ in range(5):
+            t0 = time.perf_counter()
+            OA.prefill(qf, kf, vf, 0, W, shape.scale)
+            ts.append(time.perf_counter() - t0)
+        tm = float(np.median(ts))
+        rep["cpu_baseline"] = {"kind": "oracle", "seconds": round(tm, 4), "gflops": round(flops / tm / 1e9, 3),
+                               "gbs": round(nbytes / tm / 1e9, 4), "cores": _blas_threads(),
+                               "sample": "whole workload, median of 5 oracle calls"}
+    return rep
 
+
+# ----------------------------------------------------------------------------
+# widening reports
+# ----------------------------------------------------------------------------
 
 def allocator_report(wl, reps=20):
     """SWA layer of the decode workload over explicit-release tables from the
     dual-pool allocator (HSWA_LAYER_SWA_PAGED): pages held per sequence, host
     cost of one decode step's allocator calls, and the decode call's time."""
-    import time
-
     import torch
 
     import synth
@@ -399,20 +716,11 @@ def allocator_report(wl, reps=20):
     hswa.kv_append(layer, shape, cache, kn, kn, i32(np.arange(ns + 1)), i32(ctx))
     out = torch.empty((ns, hq, d), dtype=torch.bfloat16, device="cuda")
     lens, maxc = i32(ctx + 1), int(ctx.max()) + 1
-    for _ in range(3):
-        hswa.decode(layer, shape, cache, q, lens, maxc, out)
-    ts = []
-    for _ in range(reps):
-        a, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record()
-        hswa.decode(layer, shape, cache, q, lens, maxc, out)
-        b_.record()
-        b_.synchronize()
-        ts.append(a.elapsed_time(b_))
+    ms = time_back_to_back(lambda: hswa.decode(layer, shape, cache, q, lens, maxc, out), reps)
     per_seq = [alloc.usage(b)[1] for b in range(ns)]
     full_used = alloc.usage(-1)[0]
     alloc.close()
-    return {"layer": "SWA over explicit-release tables", "swa_paged_decode_ms": round(float(np.median(ts)), 5),
+    return {"layer": "SWA over explicit-release tables", "swa_paged_decode_ms": round(ms, 5),
             "swa_pages_per_seq": [int(min(per_seq)), int(max(per_seq))],
             "swa_pages_per_seq_bound": int(-(-(W - 1) // pg) + 1),
             "full_pages_held": int(full_used), "host_us_per_decode_step": round(host_us, 1)}
@@ -483,8 +791,6 @@ def prefix_tree_report(window=128, convs=128, turns=8, turn_len=512, seed=11):
     requests match their whole history; requests that branch from an earlier
     turn find FULL KV but no intact window there and are clipped. Reports host
     cost per insert / match and the matched lengths."""
-    import time
-
     from paper_2607_13095_amd import hswa
 
     rng = np.random.default_rng(seed)
@@ -531,114 +837,14 @@ def prefix_tree_report(window=128, convs=128, turns=8, turn_len=512, seed=11):
             "host_us_per_release": round(t_rel / n_ins * 1e6, 1)}
 
 
-def stack70_report(steps=5, warmup=2):
-    """The 70-layer hybrid decode step (10 FULL + 60 SWA layers, 16 sequences at
-    a 131072-token context): every layer's pools hold its own synthetic KV
-    (86 GB of FULL pages, 12 MiB per SWA layer), and one step appends the new
-    token and decodes it in every layer. Timed eagerly and as a replayed graph
-    of the step, plus per-kind parts; also reports the pool bytes per kind."""
-    import torch
-
-    import synth
-    from paper_2607_13095_amd import hswa
-    from paper_2607_13095_amd.kvcache import LayerKV, pages_for
-
-    wl = synth.stack70_decode()
-    dev = "cuda"
-    hq, hkv, d, pg, W = wl.hq, wl.hkv, wl.head_dim, wl.page_size, wl.window
-    ns = wl.ns
-    ctx = np.asarray(wl.prefix, dtype=np.int64)
-    final = (ctx + 1).tolist()
-    maxc = int(max(final))
-    shape = hswa.Shape(hq, hkv, d, pg)
-    i32 = lambda x: torch.as_tensor(np.asarray(x, dtype=np.int32), device=dev)  # noqa: E731
-    ring = hswa.ring_pages(W, pg)
-    ws = torch.empty(max(1, hswa.decode_workspace_bytes(shape, ns, maxc)), dtype=torch.uint8, device=dev)
-    layers = []
-    for li, kind in enumerate(wl.layers):
-        layer = hswa.Layer.swa(W) if kind == "swa" else hswa.Layer.full()
-        kv = LayerKV(layer, shape, final, perm=synth.page_permutation(pages_for(layer, pg, final), wl.seed, li))
-        # cached history: every position for FULL (four sequences at a time),
-        # the positions the ring keeps for SWA
-        first = np.zeros(ns, dtype=np.int64) if kind == "full" else np.maximum(0, ctx - ring * pg)
-        for b0 in range(0, ns, 4):
-            sl = slice(b0, min(ns, b0 + 4))
-            lens = ctx[sl] - first[sl]
-            T = int(lens.sum())
-            kh = synth.torch_normal_bf16((T, hkv, d), dev, wl.seed, li, b0, synth.TAG_K)
-            vh = synth.torch_normal_bf16((T, hkv, d), dev, wl.seed, li, b0, synth.TAG_V)
-            sub = hswa.Cache(kv.k_pool, kv.v_pool, kv.block_table[sl])
-            hswa.kv_append(layer, shape, sub, kh, vh, i32(synth.cu_seqlens(lens)), i32(first[sl]))
-            del kh, vh
-        layers.append(dict(kind=kind, layer=layer, kv=kv,
-                           k_new=synth.torch_normal_bf16((ns, hkv, d), dev, wl.seed, li, 0, synth.TAG_KDEC),
-                           v_new=synth.torch_normal_bf16((ns, hkv, d), dev, wl.seed, li, 0, synth.TAG_VDEC),
-                           q=synth.torch_normal_bf16((ns, hq, d), dev, wl.seed, li, 0, synth.TAG_QDEC),
-                           out=torch.empty((ns, hq, d), dtype=torch.bfloat16, device=dev)))
-    torch.cuda.synchronize()
-    cu1, start, lens_dev = i32(np.arange(ns + 1)), i32(ctx), i32(final)
-
-    def run(kinds):
-        for L in layers:
-            if L["kind"] in kinds:
-                hswa.kv_append(L["layer"], shape, L["kv"].cache, L["k_new"], L["v_new"], cu1, start)
-                hswa.decode(L["layer"], shape, L["kv"].cache, L["q"], lens_dev, maxc, L["out"], workspace=ws)
-
-    def timed(fn, n):
-        for _ in range(warmup):
-            fn()
-        torch.cuda.synchronize()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record()
-        for _ in range(n):
-            fn()
-        b.record()
-        b.synchronize()
-        return a.elapsed_time(b) / n
-
-    step_ms = timed(lambda: run(("full", "swa")), steps)
-    full_ms = timed(lambda: run(("full",)), steps)
-    swa_ms = timed(lambda: run(("swa",)), steps)
-    graph_ms = None
-    g = torch.cuda.CUDAGraph()
-    side = torch.cuda.Stream()
-    side.wait_stream(torch.cuda.current_stream())
-    with torch.cuda.stream(side):
-        run(("full", "swa"))
-    torch.cuda.current_stream().wait_stream(side)
-    torch.cuda.synchronize()
-    with torch.cuda.graph(g):
-        run(("full", "swa"))
-    graph_ms = timed(g.replay, steps)
-    row, qo = hkv * d * 2 * 2, 2 * ns * hq * d * 2
-    nfull = sum(1 for L in layers if L["kind"] == "full")
-    nswa = len(layers) - nfull
-    full_bytes = nfull * (int(np.sum(ctx + 1)) * row + qo)
-    swa_bytes = nswa * (int(np.sum(np.minimum(W, ctx + 1))) * row + qo)
-    page_b = hswa.page_bytes(shape)
-    rep = {
-        "workload": wl.name, "layers": len(layers), "full_layers": nfull, "swa_layers": nswa,
-        "step_ms": round(step_ms, 4), "graph_step_ms": round(graph_ms, 4),
-        "step_gbs": round((full_bytes + swa_bytes) / (step_ms * 1e-3) / 1e9, 1),
-        "graph_step_gbs": round((full_bytes + swa_bytes) / (graph_ms * 1e-3) / 1e9, 1),
-        "frac_hbm": round((full_bytes + swa_bytes) / (min(step_ms, graph_ms) * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-        "full_layers_ms": round(full_ms, 4), "full_gbs": round(full_bytes / (full_ms * 1e-3) / 1e9, 1),
-        "swa_layers_ms": round(swa_ms, 4), "swa_gbs": round(swa_bytes / (swa_ms * 1e-3) / 1e9, 1),
-        "algorithmic_bytes": full_bytes + swa_bytes,
-        "pool_bytes_per_full_layer": 2 * pages_for(hswa.Layer.full(), pg, final) * page_b,
-        "pool_bytes_per_swa_layer": 2 * pages_for(hswa.Layer.swa(W), pg, final) * page_b,
-    }
-    del layers, ws, g
-    torch.cuda.empty_cache()
-    return rep
-
-
 def mixed_report(reps=10, warmup=3):
     """Mixed prefill + decode step of one SWA and one FULL layer: 8 chunks of
     4096 tokens over cached prefixes uniform in [0, 65536], plus 256 decodes with
     log-normal contexts. Per layer the step runs the chunks' prefill and append,
     then the decodes' append and decode. Reports each call's rate and the step
-    time against the sum of the calls' rooflines."""
+    time against the sum of the calls' rooflines (one stream) and against the
+    larger of the prefill and decode rooflines (the bound if the two ran
+    overlapped on two streams)."""
     import torch
 
     import synth
@@ -707,22 +913,10 @@ def mixed_report(reps=10, warmup=3):
             prefill(L)
             decode(L)
 
-    def timed(fn):
-        for _ in range(warmup):
-            fn()
-        torch.cuda.synchronize()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record()
-        for _ in range(reps):
-            fn()
-        b.record()
-        b.synchronize()
-        return a.elapsed_time(b) / reps
-
     by = {L["kind"]: L for L in layers}
-    t = {f"{what}_{k}": timed(lambda f=f, L=L: f(L)) for k, L in by.items()
+    t = {f"{what}_{k}": time_back_to_back(lambda f=f, L=L: f(L), reps, warmup) for k, L in by.items()
          for what, f in (("prefill", prefill), ("decode", decode))}
-    step_ms = timed(step)
+    step_ms = time_back_to_back(step, reps, warmup)
     row, hd = hkv * d * 2 * 2, 4 * d * hq
     flops, pbytes, dbytes = {}, {}, {}
     for k in by:
@@ -736,59 +930,84 @@ def mixed_report(reps=10, warmup=3):
         pbytes[k] = keys * row + 2 * Tp * hq * d * 2
         dkeys = int(np.sum(dec_lens)) if k == "full" else int(np.sum(np.minimum(W, dec_lens)))
         dbytes[k] = dkeys * row + 2 * ndec * hq * d * 2
-    roof = sum(max(flops[k] / (MFMA_BF16_PEAK_TFLOPS * 1e12), pbytes[k] / (HBM_PEAK_GBS * 1e9)) +
-               dbytes[k] / (HBM_PEAK_GBS * 1e9) for k in by) * 1e3
+    pre_roof = sum(max(flops[k] / (MFMA_BF16_PEAK_TFLOPS * 1e12), pbytes[k] / (HBM_PEAK_GBS * 1e9)) for k in by) * 1e3
+    dec_roof = sum(dbytes[k] / (HBM_PEAK_GBS * 1e9) for k in by) * 1e3
     rep = {
-        "workload": wl.name, "step_ms": round(step_ms, 4), "roofline_sum_ms": round(roof, 4),
-        "frac_of_roofline": round(roof / step_ms, 4),
+        "workload": wl.name, "step_ms": round(step_ms, 4),
+        "roofline_sum_ms": round(pre_roof + dec_roof, 4), "frac_of_roofline": round((pre_roof + dec_roof) / step_ms, 4),
+        "roofline_two_stream_ms": round(max(pre_roof, dec_roof), 4),
+        "frac_of_two_stream_roofline": round(max(pre_roof, dec_roof) / step_ms, 4),
         "prefill_full_ms": round(t["prefill_full"], 4),
         "prefill_full_tflops": round(flops["full"] / (t["prefill_full"] * 1e-3) / 1e12, 1),
         "prefill_swa_ms": round(t["prefill_swa"], 4),
         "decode_full_ms": round(t["decode_full"], 4),
         "decode_full_gbs": round(dbytes["full"] / (t["decode_full"] * 1e-3) / 1e9, 1),
         "decode_swa_ms": round(t["decode_swa"], 4),
-        "note": "prefill and decode call times include their kv_append",
+        "note": "back-to-back means; prefill and decode call times include their kv_append",
     }
     del layers, ws
     torch.cuda.empty_cache()
     return rep
 
 
-def extra_reports(wl, full_avg):
-    """Multi-query decode, window-safe prefix tree and explicit-release allocator reports."""
+# ----------------------------------------------------------------------------
+# main
+# ----------------------------------------------------------------------------
+
+def headline(args, flush):
+    """The 70-layer step: K timed steps after W warm-ups (the contract), the
+    FULL decode call's roofline, per-kind parts, graph replays."""
     import torch
 
-    log("[bench] multi-query decode (1 + 3 queries per sequence)")
-    mt = DecodeBench(wl, nq=4)
-    for _ in range(3):
-        mt.step()
+    log("[bench] setting up stack70_decode (86 GB of FULL pages)")
+    st = Stack70Bench()
+    for _ in range(args.warmup):
+        st.run()
     torch.cuda.synchronize()
-    mt_full = mt.time_kind_back_to_back("full", 20)
-    mt_swa = mt.time_kind_back_to_back("swa", 20)
-    mtp = {"queries_per_seq": 4, "full_ms": round(mt_full, 5), "swa_ms": round(mt_swa, 5),
-           "full_gbs": round(mt.bytes["full"] / (mt_full * 1e-3) / 1e9, 1),
-           "full_ms_vs_one_query": round(mt_full / full_avg, 3)}
-    log(f"[bench] multi-query decode: {mtp}")
-    del mt
-    torch.cuda.empty_cache()
-
-    log("[bench] window-safe prefix tree")
-    prefix_rep = prefix_tree_report()
-    log(f"[bench] prefix tree: {prefix_rep}")
-
-    log("[bench] explicit-release allocator")
-    alloc_rep = allocator_report(wl)
-    log(f"[bench] allocator: {alloc_rep}")
-
-    log("[bench] 70-layer hybrid decode step (16 x 131072 context)")
-    stack = stack70_report()
-    log(f"[bench] stack70: {stack}")
-
-    log("[bench] mixed prefill + decode step")
-    mixed = mixed_report()
-    log(f"[bench] mixed: {mixed}")
-
-    return mtp, prefix_rep, alloc_rep, stack, mixed
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(args.steps):
+        st.run()
+    stop.record()
+    torch.cuda.synchronize()
+    ms_step = start.elapsed_time(stop) / args.steps
+    value = st.bytes / (ms_step * 1e-3) / 1e9
+    log(f"[bench] stack70 step {ms_step:.4f} ms = {value:.0f} GB/s")
+    # the roofline kernel: one FULL layer's decode calls back to back
+    Lf = next(L for L in st.layers if L["kind"] == "full")
+    full_avg = time_back_to_back(lambda: st.decode(Lf), max(args.steps, 10))
+    full_gbs = st.full_layer_bytes / (full_avg * 1e-3) / 1e9
+    log(f"[bench] stack70 FULL decode call {full_avg:.4f} ms = {full_gbs:.0f} GB/s")
+    rep = {"step_ms": round(ms_step, 5), "full_decode_call_ms": round(full_avg, 5), "full_decode_gbs": round(full_gbs, 1)}
+    if not args.roofline_only:
+        Ls = next(L for L in st.layers if L["kind"] == "swa")
+        rep["full_decode_call"] = time_calls(lambda: st.decode(Lf), flush, reps=10)
+        rep["swa_decode_call"] = time_calls(lambda: st.decode(Ls), flush)
+        rep["swa_decode_call_back_to_back_ms"] = round(time_back_to_back(lambda: st.decode(Ls), 50), 5)
+        full_ms = time_back_to_back(lambda: st.run(("full",)), 3)
+        swa_ms = time_back_to_back(lambda: st.run(("swa",)), 10)
+        g_step = st.graph(("full", "swa"))
+        graph_ms = time_back_to_back(g_step.replay, args.steps)
+        del g_step
+        g_swa = st.graph(("swa",))
+        graph_swa_ms = time_back_to_back(g_swa.replay, 20)
+        del g_swa
+        swa_bytes = st.nswa * st.swa_layer_bytes
+        rep.update({
+            "graph_step_ms": round(graph_ms, 5), **{f"graph_step_{k}": v for k, v in rate(st.bytes, ms=graph_ms).items()},
+            "full_layers_ms": round(full_ms, 4), **{f"full_layers_{k}": v for k, v in
+                                                    rate(st.nfull * st.full_layer_bytes, ms=full_ms).items()},
+            "swa_layers_ms": round(swa_ms, 4), "swa_layers_graph_ms": round(graph_swa_ms, 4),
+            **{f"swa_layers_graph_{k}": v for k, v in rate(swa_bytes, ms=graph_swa_ms).items()},
+        })
+        log(f"[bench] stack70 parts: {rep}")
+    cpu = None
+    if not args.no_cpu_baseline and not args.roofline_only:
+        log("[bench] CPU baseline: oracle on a sample of the 70-layer step")
+        cpu = st.cpu_baseline(args.cpu_seconds)
+        log(f"[bench] CPU baseline: {cpu}")
+    out = dict(st=st, ms_step=ms_step, value=value, full_avg=full_avg, full_gbs=full_gbs, rep=rep, cpu=cpu)
+    return out
 
 
 def main():
@@ -806,70 +1025,100 @@ def main():
     torch.cuda.set_device(0)
     if args.copy_calibration:
         copy_calibration()
+    flush = MallFlush()
 
-    wl = synth.decode_b64()
-    log(f"[bench] setting up {wl.name}")
-    db = DecodeBench(wl)
-    for _ in range(args.warmup):
-        db.step()
-    torch.cuda.synchronize()
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record()
-    for _ in range(args.steps):
-        db.step()
-    stop.record()
-    torch.cuda.synchronize()
-    total_ms = start.elapsed_time(stop)
-    ms_step = total_ms / args.steps
-    dec_bytes = sum(db.bytes.values())
-    value = dec_bytes / (ms_step * 1e-3) / 1e9
-    # The roofline kernel alone: FULL-layer decode calls back to back on the
-    # stream they run on, one HIP event pair around them (no host gap per call).
-    full_avg = db.time_kind_back_to_back("full", max(args.steps, 10))
-    full_gbs = db.bytes["full"] / (full_avg * 1e-3) / 1e9
-    swa_ms = db.time_kind("swa")
-    log(f"[bench] decode step {ms_step:.4f} ms; FULL decode {full_avg:.4f} ms ({full_gbs:.0f} GB/s); "
-        f"SWA decode {swa_ms:.4f} ms")
+    h = headline(args, flush)
+    st = h["st"]
+    wl = st.wl
+    stack = {"workload": wl.name, "layers": len(st.layers), "full_layers": st.nfull, "swa_layers": st.nswa,
+             "algorithmic_bytes": st.bytes, "pool_bytes_per_full_layer": st.pool_bytes["full_layer"],
+             "pool_bytes_per_swa_layer": st.pool_bytes["swa_layer"], **h["rep"]}
+    full_layer_bytes = st.full_layer_bytes
+    del h["st"], st
+    torch.cuda.empty_cache()
+
+    decode_b64 = None
+    if not args.roofline_only:
+        dw = synth.decode_b64()
+        log(f"[bench] setting up {dw.name}")
+        db = DecodeBench(dw)
+        d_step = time_back_to_back(db.step, 20, warmup=5)
+        d_full = time_back_to_back(lambda: db.decode(db.kind("full")), 20)
+        decode_b64 = {
+            "workload": dw.name, "step_ms": round(d_step, 5),
+            **{f"step_{k}": v for k, v in rate(sum(db.bytes.values()), ms=d_step).items()},
+            "full_decode_ms": round(d_full, 5), **{f"full_{k}": v for k, v in rate(db.bytes["full"], ms=d_full).items()},
+            "full_decode_call": time_calls(lambda: db.decode(db.kind("full")), flush),
+            "swa_decode_call": time_calls(lambda: db.decode(db.kind("swa")), flush),
+            "swa_decode_back_to_back_ms": round(time_back_to_back(lambda: db.decode(db.kind("swa")), 50), 5),
+            "decode_bytes": db.bytes,
+        }
+        if not args.no_cpu_baseline:
+            decode_b64["cpu_baseline"] = db.cpu_baseline(5.0)
+        log(f"[bench] decode_b64: {decode_b64}")
+        mtp_wl = dw
+        del db
+        torch.cuda.empty_cache()
+
+    swa512 = None
+    if not args.roofline_only:
+        log("[bench] swa_prefill_512")
+        swa512 = swa512_report(flush, cpu=not args.no_cpu_baseline)
+        log(f"[bench] swa_prefill_512: {swa512}")
 
     prefill = None
     if not args.no_prefill:
         pw = synth.chunked_prefill_4x8k()
         log(f"[bench] setting up {pw.name}")
         pb = PrefillBench(pw)
-        f_ms = pb.time_kind("full")
-        s_ms = pb.time_kind("swa")
+        Lf, Ls = pb.kind("full"), pb.kind("swa")
+        f_ms = time_back_to_back(lambda: pb.call(Lf), 20, warmup=10)
+        s_ms = time_back_to_back(lambda: pb.call(Ls), 20, warmup=10)
         f_tf = pb.flops["full"] / (f_ms * 1e-3) / 1e12
-        s_gbs = pb.bytes["swa"] / (s_ms * 1e-3) / 1e9
         prefill = {
-            "workload": pw.name, "full_ms": round(f_ms, 4), "full_tflops": round(f_tf, 2),
-            "full_frac_mfma": round(f_tf / MFMA_BF16_PEAK_TFLOPS, 4),
-            "swa_ms": round(s_ms, 4), "swa_gbs": round(s_gbs, 1), "swa_frac_hbm": round(s_gbs / HBM_PEAK_GBS, 4),
-            "swa_tflops": round(pb.flops["swa"] / (s_ms * 1e-3) / 1e12, 2),
+            "workload": pw.name, "full_ms": round(f_ms, 4), **{f"full_{k}": v for k, v in
+                                                              rate(pb.bytes["full"], pb.flops["full"], f_ms).items()},
+            "swa_ms": round(s_ms, 4), **{f"swa_{k}": v for k, v in rate(pb.bytes["swa"], pb.flops["swa"], s_ms).items()},
             "roofline": {"bound": "mfma", "achieved": round(f_tf, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
                          "unit": "TFLOP/s", "frac": round(f_tf / MFMA_BF16_PEAK_TFLOPS, 4),
                          "traffic": measured_traffic("prefill_full"), "algorithmic_bytes": pb.bytes["full"],
-                         "algorithmic_flops": pb.flops["full"]},
+                         "algorithmic_flops": pb.flops["full"], "kernel": "prefill_kernel (FULL layer call)"},
         }
-        log(f"[bench] prefill FULL {f_ms:.3f} ms = {f_tf:.1f} TFLOP/s; SWA {s_ms:.3f} ms = {s_gbs:.0f} GB/s")
+        log(f"[bench] prefill FULL {f_ms:.3f} ms = {f_tf:.1f} TFLOP/s; SWA {s_ms:.4f} ms")
         if not args.roofline_only:
+            prefill["full_call"] = time_calls(lambda: pb.call(Lf), flush)
+            prefill["swa_call"] = time_calls(lambda: pb.call(Ls), flush)
             log("[bench] layerwise prefetch (70-layer prefill stack, prefix from pinned host memory)")
             prefill["prefetch"] = prefetch_report(pb)
             log(f"[bench] prefetch: {prefill['prefetch']}")
+            if not args.no_cpu_baseline:
+                log("[bench] prefill CPU baseline")
+                prefill["cpu_baseline"] = pb.cpu_baseline()
+                log(f"[bench] prefill CPU baseline: {prefill['cpu_baseline']}")
         del pb
         torch.cuda.empty_cache()
 
-    mtp = prefix_rep = alloc_rep = stack = mixed = cpu = None
-    if args.roofline_only:
-        args.no_cpu_baseline = True
-    else:
-        mtp, prefix_rep, alloc_rep, stack, mixed = extra_reports(wl, full_avg)
+    mtp = prefix_rep = alloc_rep = mixed = None
+    if not args.roofline_only:
+        log("[bench] multi-query decode (1 + 3 queries per sequence)")
+        mt = DecodeBench(mtp_wl, nq=4)
+        mt_full = time_back_to_back(lambda: mt.decode(mt.kind("full")), 20, warmup=3)
+        mt_swa = time_back_to_back(lambda: mt.decode(mt.kind("swa")), 20, warmup=3)
+        mtp = {"queries_per_seq": 4, "full_ms": round(mt_full, 5), "swa_ms": round(mt_swa, 5),
+               "full_gbs": round(mt.bytes["full"] / (mt_full * 1e-3) / 1e9, 1),
+               "full_ms_vs_one_query": round(mt_full / decode_b64["full_decode_ms"], 3)}
+        log(f"[bench] multi-query decode: {mtp}")
+        del mt
+        torch.cuda.empty_cache()
+        log("[bench] window-safe prefix tree")
+        prefix_rep = prefix_tree_report()
+        log("[bench] explicit-release allocator")
+        alloc_rep = allocator_report(mtp_wl)
+        log("[bench] mixed prefill + decode step")
+        mixed = mixed_report()
+        log(f"[bench] mixed: {mixed}")
 
-    if not args.no_cpu_baseline:
-        log("[bench] CPU baseline (oracle)")
-        cpu = db.cpu_baseline(args.cpu_seconds)
-
-
+    ms_step, value = h["ms_step"], h["value"]
     line = {
         "metric": "decode attn HBM GB/s (% peak) + prefill attn TFLOP/s (% MFMA), W=128",
         "value": round(value, 2),
@@ -883,22 +1132,24 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": wl.name, "sequences": wl.ns, "context": "uniform [1024, 32768] cached tokens",
-                   "layers": "1 SWA (W=128) + 1 FULL", "q_heads": wl.hq, "kv_heads": wl.hkv,
-                   "head_dim": wl.head_dim, "page_size": wl.page_size, "frac_hbm": round(value / HBM_PEAK_GBS, 4),
-                   "decode_bytes": dec_bytes, "full_decode_ms": round(full_avg, 5),
-                   "swa_decode_ms": round(swa_ms, 5)},
-        "roofline": {"bound": "hbm", "achieved": round(full_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(full_gbs / HBM_PEAK_GBS, 4), "traffic": measured_traffic("decode_full"),
-                     "algorithmic_bytes": db.bytes["full"],
-                     "kernel": "FULL-layer decode call: decode_kernel<true,true> + decode_merge_kernel"},
+        "config": {"workload": wl.name, "sequences": wl.ns, "context": "131072 cached tokens",
+                   "layers": "70: 60 SWA (W=128) + 10 FULL (FULL iff layer % 7 == 6)", "q_heads": wl.hq,
+                   "kv_heads": wl.hkv, "head_dim": wl.head_dim, "page_size": wl.page_size,
+                   "frac_hbm": round(value / HBM_PEAK_GBS, 4), "decode_bytes": stack["algorithmic_bytes"]},
+        "roofline": {"bound": "hbm", "achieved": round(h["full_gbs"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(h["full_gbs"] / HBM_PEAK_GBS, 4),
+                     "traffic": measured_traffic("decode_full_stack70"), "algorithmic_bytes": full_layer_bytes,
+                     "kernel": "FULL-layer decode call of the 70-layer step: decode_kernel<true,true,1> + "
+                               "decode_merge_kernel"},
+        "stack70_decode": stack,
+        "decode_b64": decode_b64,
+        "swa_prefill_512": swa512,
         "prefill": prefill,
         "multi_query_decode": mtp,
         "allocator": alloc_rep,
         "prefix_tree": prefix_rep,
-        "stack70_decode": stack,
         "mixed_step": mixed,
-        "cpu_baseline": cpu,
+        "cpu_baseline": h["cpu"],
     }
     print(json.dumps(line), flush=True)
 
