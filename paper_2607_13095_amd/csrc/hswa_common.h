@@ -31,6 +31,19 @@ __device__ __forceinline__ u32x4 ldg128(const void *p) {
 
 __device__ __forceinline__ void stg128(void *p, u32x4 v) { *reinterpret_cast<u32x4 *>(p) = v; }
 
+// 16-byte load through the global address space, for a source pointer chosen
+// at run time between buffers (which would otherwise become a flat load, one
+// that also counts against the LDS wait counter).
+typedef __attribute__((address_space(1))) const u32x4 global_u32x4;
+__device__ __forceinline__ u32x4 ldg128_global(const void *p) { return *(global_u32x4 *)p; }
+
+// Bits i (0 .. 7) of the keys k0 + i inside [lo, hi].
+__device__ __forceinline__ uint32_t key_range_bits(int k0, int lo, int hi) {
+  const int a = min(max(lo - k0, 0), 8);
+  const int z = min(max(hi - k0 + 1, 0), 8);
+  return ((1u << z) - 1u) & ~((1u << a) - 1u);
+}
+
 // Element offset in the K pool of (page, KV head g, in-page key offset o, dim d).
 // In a block of B = 2^vb_shift keys, key k sits in half (k >> 2) & 1 at row
 // ((k >> 3) << 2) | (k & 3); dim d in slab d >> 5, 16-byte piece (d >> 3) & 3.

@@ -71,6 +71,15 @@ struct PrefillParams {
 hipError_t launch_kv_append(const AppendParams &p, hipStream_t stream);
 hipError_t launch_decode(const DecodeParams &p, hipStream_t stream);
 hipError_t launch_prefill(const PrefillParams &p, hipStream_t stream);
+// SWA prefill whose window is at most kPrefillWindowMax keys: 128 query rows
+// per workgroup over the window's keys only (prefill_window.hip).
+constexpr int kPrefillWindowMax = 512;
+hipError_t launch_prefill_window(const PrefillParams &p, hipStream_t stream);
+// SWA prefill with a GQA group of at least 8 and W + 256 / G - 1 <= 160: one
+// workgroup per run of position tiles, the window's chunks in an LDS ring
+// (prefill_run.hip).
+bool prefill_run_fits(const PrefillParams &p);
+hipError_t launch_prefill_run(const PrefillParams &p, hipStream_t stream);
 
 // Device address of the library's fixed scratch array on the current device
 // (looked up once per device).

@@ -606,6 +606,8 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
 
 hipError_t launch_prefill(const PrefillParams &p, hipStream_t stream) {
   if (p.ns <= 0 || p.max_chunk_len <= 0 || p.total_tokens <= 0) return hipSuccess;
+  if (p.pool.window > 0 && prefill_run_fits(p)) return launch_prefill_run(p, stream);
+  if (p.pool.window > 0 && p.pool.window <= kPrefillWindowMax) return launch_prefill_window(p, stream);
   const int npos = kRows / p.group;
   const int64_t ntq = (p.max_chunk_len + npos - 1) / npos;
   const int64_t pairs_per_xcd = ((int64_t)p.ns * p.hkv + kXcds - 1) / kXcds;

@@ -1,0 +1,430 @@
+// Windowed (SWA) chunked prefill, persistent over runs of position tiles.
+//
+// "Compute Analysis": an SWA layer's attention covers a local window, so its
+// prefill is bound by moving q, o and the chunk's K/V rather than by the
+// matrix cores. A workgroup that serves one tile of positions has to stage the
+// whole window (W + positions - 1 keys) for that tile alone, so every key is
+// staged about W / positions times. Here one workgroup (8 waves) walks a run
+// of consecutive tiles of one (sequence, KV head) pair instead: tile t holds
+// 256 query rows (a row = a (position, query head) pair of the KV head's GQA
+// group, so 256 / G positions), the window's 32-key chunks stay in an LDS ring
+// of eight, and each tile stages only the chunk its last positions add. The
+// chunk a tile will need next is loaded into registers while the tile
+// computes; each wave loads its next tile's queries as soon as its last QK^T
+// of the tile has read the current ones; waves run through a tile's chunks
+// without barriers (one barrier per tile).
+//
+// Used when G >= 8 and W + 256 / G - 1 <= 160: a tile then spans at most 7
+// chunks and the next tile adds at most one, so the ring of 8 is never short.
+// Per 32-key chunk and wave (bf16 MFMA, fp32 accumulate), as in the other
+// prefill kernels:
+//   S^T[key][row] = K[key][:] . Q[row][:]     (Q held in registers)
+//   online softmax per row (exp2, scale * log2 e folded in, running maximum in
+//   exp2 units, raised lazily)
+//   O^T[d][row]  += V^T[d][key] . P^T[key][row]
+// LDS holds each chunk in MFMA operand order (K: the pool's K block layout;
+// V^T: block dt for lane r + 16 q = keys 8 q .. +7 of dim 16 dt + r). Cached
+// keys are chunked at 32-aligned positions and the chunk's own keys from P
+// on, so no chunk mixes the two sources; keys outside the run's range are
+// staged as zeros and every column masks its own window.
+#include <algorithm>
+#include <cfloat>
+
+#include "hswa_common.h"
+#include "hswa_launch.h"
+
+namespace hswa {
+namespace {
+
+constexpr int kRThreads = 512;
+constexpr int kRRows = 256;                      // query rows per tile (8 waves x 32)
+constexpr int kRChunk = 32;                      // keys per chunk
+constexpr int kRBufs = 8;                        // LDS ring of chunks
+constexpr int kRKBytes = kRChunk * kHeadDim * 2; // 8 KiB of K per chunk
+constexpr int kRBufBytes = 2 * kRKBytes;         // K, then V^T
+constexpr int kRCG = 2;                          // 16-column MFMA groups per wave
+constexpr float kRLaneSumLimit = 4096.f;         // lane share of a row sum that raises the maximum
+constexpr int kRTargetGroups = 256;              // workgroups a launch aims for (one per CU)
+
+// Staging registers of one chunk: waves 0-3 carry its V (two 16-byte pieces a
+// thread), waves 4-7 its K (two pieces a thread).
+struct RStage {
+  u32x4 a[2];
+  uint32_t keep;  // K: bit i = piece i holds data; V: bits 8 i .. 8 i + 7 = its keys that do
+};
+
+__global__ __launch_bounds__(kRThreads) __attribute__((amdgpu_waves_per_eu(2))) void prefill_run_kernel(
+    PrefillParams p) {
+  __shared__ __attribute__((aligned(16))) unsigned char s_lds[kRBufs * kRBufBytes];
+
+  const PoolView &pv = p.pool;
+  const int G = p.group;
+  const int npos = kRRows / G;  // positions per tile
+  const int ntq = (p.max_chunk_len + npos - 1) / npos;
+  const int npairs = p.ns * p.hkv;
+  const int runs = (int)(gridDim.x / npairs);
+  const int tpr = (ntq + runs - 1) / runs;  // tiles per run
+  const int pair = (int)(blockIdx.x / runs), run = (int)(blockIdx.x % runs);
+  if (pair >= npairs) return;
+  const int b = pair / p.hkv, g = pair - b * p.hkv;
+
+  const int tok0 = p.cu_seqlens[b];
+  const int C = min(min(p.cu_seqlens[b + 1], p.total_tokens) - tok0, p.max_chunk_len);
+  const int P = p.prefix_lens[b];
+  const int t0 = run * tpr;
+  const int t1 = min((C + npos - 1) / npos, t0 + tpr);
+  if (t0 >= t1 || P < 0 || tok0 < 0) return;
+  const int W = pv.window;
+  // keys of the whole run, cut at P into cached chunks (32-aligned) and new ones (aligned to P)
+  const int klo = max(0, P + t0 * npos - W + 1);
+  const int khi = P + min(C, t1 * npos) - 1;
+  const int chi = min(P - 1, khi);  // last cached key (< klo: none)
+  const int ncached = klo <= chi ? (chi >> 5) - (klo >> 5) + 1 : 0;
+  const int nbase = max(klo, P) - P;
+  const int nnew = khi >= max(klo, P) ? ((khi - P) >> 5) - (nbase >> 5) + 1 : 0;
+  const int nch = ncached + nnew;
+  auto chunk_base = [&](int c) {
+    return c < ncached ? (klo & ~(kRChunk - 1)) + kRChunk * c : P + kRChunk * ((nbase >> 5) + c - ncached);
+  };
+  auto chunk_of = [&](int key) {
+    return key < P ? (key >> 5) - (klo >> 5) : ncached + ((key - P) >> 5) - (nbase >> 5);
+  };
+
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int r = lane & 15, q = lane >> 4;
+  const int hkv = p.hkv, hq = p.hq;
+  const int shift = pv.pg_shift, pg = 1 << shift;
+  const float c2 = p.scale_log2;
+
+  // Page ids of the run's cached keys (at most W - 1 <= 159 keys, 12 pages of
+  // 16): lane i holds the physical page of logical page lp0 + i, -1 if not
+  // cached or not a valid page.
+  const int lp0 = (klo & ~(kRChunk - 1)) >> shift;
+  int tab = -1;
+  if (ncached > 0) {
+    const int lp = lp0 + lane;
+    if (lp <= (chi >> shift)) {
+      const int e = pv.ring > 0 ? lp % pv.ring : lp;
+      if (e < pv.stride) {
+        const int64_t v = pv.table[(int64_t)b * pv.stride + e];
+        tab = (v >= 0 && v < pv.num_pages) ? (int)v : -1;
+      }
+    }
+  }
+  auto page_at = [&](int j) { return __shfl(tab, (j >> shift) - lp0, kWave); };
+
+  // ---- staging ----
+  // K piece idx (0 .. 511) of a chunk: dims 32 t + 8 qq .. +7 (t = (idx >> 6) & 3,
+  // qq = (idx >> 4) & 3) of chunk key 8 ((idx & 15) >> 2) + 4 (idx >> 8) + (idx & 3),
+  // at byte 16 idx of the K block. V^T piece idx: keys 8 qq .. +7 of dim
+  // 16 (idx >> 6) + (idx & 15), at byte 16 idx of the V^T block.
+  auto k_key = [](int idx) { return ((idx & 15) >> 2) * 8 + (idx >> 8) * 4 + (idx & 3); };
+  auto k_dim = [](int idx) { return ((idx >> 6) & 3) * 32 + ((idx >> 4) & 3) * 8; };
+  auto v_dim = [](int idx) { return (idx >> 6) * 16 + (idx & 15); };
+  auto v_keys = [](int idx) { return ((idx >> 4) & 3) * 8; };
+  const u32x4 zero = {0u, 0u, 0u, 0u};
+  const bool vwave = wave < 4;          // waves 0-3 stage V, waves 4-7 stage K
+  const int st_tid = tid & 255;         // thread index within its half
+  auto fetch = [&](int c, RStage &st) {
+    c = min(c, nch - 1);  // past the end: a repeat of the last chunk, never stored
+    const int kb = chunk_base(c);
+    const bool cached = c < ncached;
+    const uint16_t *src[2];
+    uint32_t keep = 0u;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int idx = st_tid + 256 * i;
+      if (vwave) {
+        if (cached) {
+          const int j0 = kb + v_keys(idx);
+          const int page = page_at(j0);
+          src[i] = pv.v_pool + v_offset(pv, page >= 0 ? page : 0, hkv, g, j0 & (pg - 1), v_dim(idx));
+          keep |= (page >= 0 ? key_range_bits(j0, klo, chi) : 0u) << (8 * i);
+        } else {
+          // a row piece: key 8 wave + 4 i + lane / 16, dims 8 (lane % 16) .. +7
+          const int jv = kb + 8 * wave + 4 * i + (lane >> 4);
+          const bool in = jv >= klo && jv <= khi;
+          src[i] = p.v_new + ((int64_t)(tok0 + (in ? jv - P : 0)) * hkv + g) * kHeadDim + (lane & 15) * 8;
+          keep |= (in ? 0xFFu : 0u) << (8 * i);
+        }
+      } else {
+        const int j = kb + k_key(idx);
+        if (cached) {
+          const int page = page_at(j);
+          const bool in = j >= klo && j <= chi && page >= 0;
+          src[i] = pv.k_pool + k_offset(pv, in ? page : 0, hkv, g, j & (pg - 1), k_dim(idx));
+          keep |= (in ? 1u : 0u) << i;
+        } else {
+          const bool in = j >= klo && j <= khi;
+          src[i] = p.k_new + ((int64_t)(tok0 + (in ? j - P : 0)) * hkv + g) * kHeadDim + k_dim(idx);
+          keep |= (in ? 1u : 0u) << i;
+        }
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) st.a[i] = ldg128_global(src[i]);
+    st.keep = keep;
+  };
+  auto lds128 = [&](uint32_t off) { return reinterpret_cast<u32x4 *>(s_lds + off); };
+  auto buf_off = [&](int buf) { return (uint32_t)__builtin_amdgcn_readfirstlane(buf * kRBufBytes); };
+  // V^T bytes of dims 8 (lane % 16) + 2 (lane / 16) and + 1, keys 8 wave .. +7
+  const uint32_t st_vrow = kRKBytes + ((((8 * (lane & 15)) >> 4) * 64 + ((8 * (lane & 15) + 2 * (lane >> 4)) & 15) +
+                                        16 * (wave & 3)) * 16);
+  // 4 x 4 transpose of dwords across the lanes l, l ^ 16, l ^ 32, l ^ 48.
+  auto transpose4 = [&](const u32x4 &t, uint32_t (&w)[4]) {
+    const auto a = __builtin_amdgcn_permlane32_swap(t[0], t[2], false, false);
+    const auto bb = __builtin_amdgcn_permlane32_swap(t[1], t[3], false, false);
+    const auto cc = __builtin_amdgcn_permlane16_swap((uint32_t)a[0], (uint32_t)bb[0], false, false);
+    const auto d = __builtin_amdgcn_permlane16_swap((uint32_t)a[1], (uint32_t)bb[1], false, false);
+    w[0] = (uint32_t)cc[0];
+    w[1] = (uint32_t)cc[1];
+    w[2] = (uint32_t)d[0];
+    w[3] = (uint32_t)d[1];
+  };
+  auto store = [&](int c, const RStage &st0) {
+    const bool cached = c < ncached;
+    const uint32_t bo = buf_off(c % kRBufs);
+    RStage st = st0;
+    if (!vwave) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        st.a[i] = (st.keep >> i) & 1u ? st.a[i] : zero;
+        *lds128(bo + 16 * (st_tid + 256 * i)) = st.a[i];
+      }
+    } else if (cached) {
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const uint32_t k8 = (st.keep >> (8 * i)) & 0xFFu;
+        if (k8 != 0xFFu) st.a[i] = keep_bf16x8(st.a[i], k8);
+        *lds128(bo + kRKBytes + 16 * (st_tid + 256 * i)) = st.a[i];
+      }
+    } else {
+      // lanes l % 16 + 16 m hold keys 8 wave + 4 i + m (piece i) x dims
+      // 8 (l % 16) .. +7; after the transposes lane m holds dims 2 m, 2 m + 1 of
+      // keys 8 wave .. +7, split into one V^T piece per dim
+#pragma unroll
+      for (int i = 0; i < 2; ++i) st.a[i] = (st.keep >> (8 * i)) & 1u ? st.a[i] : zero;
+      uint32_t w[8];
+      transpose4(st.a[0], *reinterpret_cast<uint32_t(*)[4]>(&w[0]));
+      transpose4(st.a[1], *reinterpret_cast<uint32_t(*)[4]>(&w[4]));
+      u32x4 lo, hi;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        lo[j] = __builtin_amdgcn_perm(w[2 * j + 1], w[2 * j], 0x05040100u);
+        hi[j] = __builtin_amdgcn_perm(w[2 * j + 1], w[2 * j], 0x07060302u);
+      }
+      *lds128(bo + st_vrow) = lo;
+      *lds128(bo + st_vrow + 16) = hi;
+    }
+  };
+
+  // ---- per-tile state ----
+  u32x4 qf[kRCG][4];
+  int cpos[kRCG], clo[kRCG];
+  bool cval[kRCG];
+  float m[kRCG], lsum[kRCG];  // m: running maximum in exp2 units
+  f32x4 acc[kRCG][8];
+  auto load_q = [&](int t) {
+    const int q0 = t * npos, q1 = min(C, q0 + npos) - 1;
+#pragma unroll
+    for (int cg = 0; cg < kRCG; ++cg) {
+      const int row = wave * (16 * kRCG) + cg * 16 + r;
+      const int po = row / G, head = row - po * G;
+      const bool ok = q0 + po <= q1;
+      const int64_t tok = tok0 + q0 + (ok ? po : 0);
+      const uint16_t *qrow = p.q + (tok * hq + (int64_t)g * G + head) * kHeadDim;
+#pragma unroll
+      for (int t4 = 0; t4 < 4; ++t4) qf[cg][t4] = ldg128(qrow + 32 * t4 + 8 * q);
+    }
+  };
+
+  const uint32_t op_lane = lane * 16;
+  // One chunk: QK^T, masks, online softmax (lazy maximum, exact), PV. With
+  // `prefetch`, the next tile's queries are loaded right after the QK^T.
+  // `first`: the wave's first chunk of the tile; its maximum is formed exactly
+  // at once (the lazy check would always fail on it).
+  auto chunk = [&](int c, int kb, int kend, int wint_lo, int wint_hi, bool first, bool prefetch, int tnext) {
+    const uint32_t a = buf_off(c % kRBufs) + op_lane;
+    f32x4 sc[2][kRCG];
+#pragma unroll
+    for (int ab = 0; ab < 2; ++ab)
+#pragma unroll
+      for (int cg = 0; cg < kRCG; ++cg) sc[ab][cg] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const u32x4 ka = *lds128(a + 1024 * t);
+      const u32x4 kbv = *lds128(a + 4096 + 1024 * t);
+#pragma unroll
+      for (int cg = 0; cg < kRCG; ++cg) {
+        sc[0][cg] = mfma16x16x32(ka, qf[cg][t], sc[0][cg]);
+        sc[1][cg] = mfma16x16x32(kbv, qf[cg][t], sc[1][cg]);
+      }
+    }
+    if (prefetch) load_q(tnext);
+    u32x4 vf[8];
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) vf[dt] = *lds128(a + kRKBytes + 1024 * dt);
+    if (!(kb >= wint_lo && kb + kRChunk - 1 <= min(wint_hi, kend))) {
+      const int j0 = kb + 8 * q;  // this lane's keys are kb + 8 q + e, e = 4 ab + i
+#pragma unroll
+      for (int cg = 0; cg < kRCG; ++cg) {
+        const int lo_e = max(clo[cg] - j0, 0);
+        const int hi_e = min(min(cpos[cg], kend) - j0, 7);
+        const uint32_t bits = hi_e < lo_e ? 0u : ((2u << hi_e) - 1u) & ~((1u << lo_e) - 1u);
+#pragma unroll
+        for (int ab = 0; ab < 2; ++ab)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) sc[ab][cg][i] = (bits >> (4 * ab + i)) & 1u ? sc[ab][cg][i] : -INFINITY;
+      }
+    }
+    u32x4 pf[kRCG];
+    float ts[kRCG];
+    auto exps = [&]() {
+#pragma unroll
+      for (int cg = 0; cg < kRCG; ++cg) {
+        float pr[8];
+#pragma unroll
+        for (int ab = 0; ab < 2; ++ab)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) pr[4 * ab + i] = fast_exp2(fmaf(sc[ab][cg][i], c2, -m[cg]));
+        ts[cg] = 0.f;
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) {
+          pf[cg][jj] = pack_bf16x2(pr[2 * jj], pr[2 * jj + 1]);
+          ts[cg] = dot2_bf16_ones(pf[cg][jj], ts[cg]);
+        }
+      }
+    };
+    bool raise = first;
+    if (!first) {
+      exps();
+#pragma unroll
+      for (int cg = 0; cg < kRCG; ++cg) raise = raise || !(ts[cg] <= kRLaneSumLimit);
+    }
+    if (__builtin_amdgcn_ballot_w64(raise) != 0) {
+#pragma unroll
+      for (int cg = 0; cg < kRCG; ++cg) {
+        const float a8[8] = {sc[0][cg][0], sc[0][cg][1], sc[0][cg][2], sc[0][cg][3],
+                             sc[1][cg][0], sc[1][cg][1], sc[1][cg][2], sc[1][cg][3]};
+        const float cmax = max_xor32(max_xor16(max8(a8))) * c2;
+        const bool up = cmax > m[cg];
+        const float alpha = up ? fast_exp2(m[cg] - cmax) : 1.f;
+        m[cg] = up ? cmax : m[cg];
+        lsum[cg] *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < 8; ++dt) acc[cg][dt] *= alpha;
+      }
+      exps();
+    }
+#pragma unroll
+    for (int cg = 0; cg < kRCG; ++cg) lsum[cg] += ts[cg];
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt)
+#pragma unroll
+      for (int cg = 0; cg < kRCG; ++cg) acc[cg][dt] = mfma16x16x32(vf[dt], pf[cg], acc[cg][dt]);
+  };
+
+  // ---- warm-up: the chunks of the first tile, two stages in flight ----
+  auto tile_last_key = [&](int t) { return P + min(C, (t + 1) * npos) - 1; };
+  RStage sa, sb;
+  const int ce0 = chunk_of(tile_last_key(t0));
+  for (int c = 0; c <= ce0; c += 2) {
+    fetch(c, sa);
+    fetch(c + 1, sb);
+    store(c, sa);
+    if (c + 1 <= ce0) store(c + 1, sb);
+  }
+  int stored = ce0 + 1;  // next chunk to store
+  fetch(stored, sa);     // the chunk the next tile adds
+  load_q(t0);
+
+  for (int t = t0; t < t1; ++t) {
+    const int q0 = t * npos, q1 = min(C, q0 + npos) - 1;
+    __syncthreads();
+#pragma unroll
+    for (int cg = 0; cg < kRCG; ++cg) {
+      const int row = wave * (16 * kRCG) + cg * 16 + r;
+      const int po = row / G;
+      cval[cg] = q0 + po <= q1;
+      cpos[cg] = P + q0 + po;
+      clo[cg] = max(0, cpos[cg] - W + 1);
+      m[cg] = -FLT_MAX;
+      lsum[cg] = 0.f;
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) acc[cg][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    // this wave's rows: positions po_lo .. po_hi of the tile
+    const int po_lo = (wave * 16 * kRCG) / G;
+    const int po_hi = min((wave * 16 * kRCG + 16 * kRCG - 1) / G, q1 - q0);
+    const bool more = t + 1 < t1;
+    if (po_lo <= q1 - q0) {
+      const int wklo = max(0, P + q0 + po_lo - W + 1), wkhi = P + q0 + po_hi;
+      const int wint_lo = max(0, P + q0 + po_hi - W + 1), wint_hi = P + q0 + po_lo;
+      const int cw0 = chunk_of(wklo), cw1 = chunk_of(wkhi);
+      // the last chunk is peeled off: only it overwrites the queries (with the
+      // next tile's; on the run's last tile a harmless reload of this one), so
+      // the loop keeps them in place
+      for (int c = cw0; c < cw1; ++c)
+        chunk(c, chunk_base(c), c < ncached ? chi : khi, wint_lo, wint_hi, c == cw0, false, 0);
+      chunk(cw1, chunk_base(cw1), cw1 < ncached ? chi : khi, wint_lo, wint_hi, cw1 == cw0, true,
+            more ? t + 1 : t);
+    } else if (more) {
+      load_q(t + 1);
+    }
+    // normalise this tile's rows
+    u32x2 wo[kRCG][8];
+#pragma unroll
+    for (int cg = 0; cg < kRCG; ++cg) {
+      const float l = sum_xor32(sum_xor16(lsum[cg]));
+      const float inv = 1.f / l;
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) {
+        wo[cg][dt][0] = pack_bf16x2(acc[cg][dt][0] * inv, acc[cg][dt][1] * inv);
+        wo[cg][dt][1] = pack_bf16x2(acc[cg][dt][2] * inv, acc[cg][dt][3] * inv);
+      }
+    }
+    // Stage the chunk the next tile adds now, before this tile's output stores
+    // (its loads went out a tile ago; a wait for them then never waits for the
+    // stores). Its buffer held a chunk that ends before this tile's range, so
+    // waves still computing this tile are not disturbed; the barrier that
+    // opens the next tile makes it visible.
+    if (more) {
+      const int ce_next = chunk_of(tile_last_key(t + 1));
+      while (stored <= ce_next) {
+        store(stored, sa);
+        ++stored;
+        fetch(stored, sa);
+      }
+    }
+    // write this tile's rows
+#pragma unroll
+    for (int cg = 0; cg < kRCG; ++cg) {
+      if (!cval[cg]) continue;
+      const int row = wave * (16 * kRCG) + cg * 16 + r;
+      const int po = row / G, head = row - po * G;
+      uint16_t *orow = p.out + ((int64_t)(tok0 + q0 + po) * hq + (int64_t)g * G + head) * kHeadDim;
+#pragma unroll
+      for (int dt = 0; dt < 8; ++dt) *reinterpret_cast<u32x2 *>(orow + 16 * dt + 4 * q) = wo[cg][dt];
+    }
+  }
+}
+
+}  // namespace
+
+bool prefill_run_fits(const PrefillParams &p) {
+  const int npos = kRRows / p.group;
+  return p.group >= 8 && p.pool.window > 0 && p.pool.window + npos - 1 <= 160;
+}
+
+hipError_t launch_prefill_run(const PrefillParams &p, hipStream_t stream) {
+  if (p.ns <= 0 || p.max_chunk_len <= 0 || p.total_tokens <= 0) return hipSuccess;
+  const int npos = kRRows / p.group;
+  const int64_t ntq = (p.max_chunk_len + npos - 1) / npos;
+  const int64_t npairs = (int64_t)p.ns * p.hkv;
+  const int64_t runs = std::max<int64_t>(1, std::min<int64_t>(ntq, (kRTargetGroups + npairs - 1) / npairs));
+  return launch_kernel(prefill_run_kernel, dim3((unsigned)(npairs * runs)), dim3(kRThreads), stream, p);
+}
+
+}  // namespace hswa

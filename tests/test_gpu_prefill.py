@@ -89,3 +89,19 @@ def test_prefill_large_scale(gpu_lib, scale):
     for kind, window in (("swa", 128), ("full", 0)):
         gpu, ref, _ = run_prefill(kind, window, 64, 64, 8, [1000, 3], [2048, 700], (304, 2), scale=scale)
         assert_close(gpu, ref, f"{kind} prefill over a prefix, scale {scale}")
+
+
+@pytest.mark.parametrize("hq,hkv,window", [(64, 8, 129), (64, 8, 130), (128, 8, 145), (128, 8, 146),
+                                           (32, 8, 512), (32, 8, 513), (64, 8, 33)])
+def test_prefill_window_kernel_boundaries(gpu_lib, hq, hkv, window):
+    """SWA prefill takes one of three kernels: with a GQA group G >= 8 and
+    W + 256 / G - 1 <= 160 the persistent one over runs of tiles, otherwise up
+    to W = 512 the per-tile windowed one, and beyond that the FULL-style one.
+    Each side of both limits, over prefixes that put window starts before,
+    across and after the prefix / chunk boundary (PG 16 and 64), against the
+    oracle."""
+    print(f"[prefill-boundaries] hq={hq} hkv={hkv} W={window}", flush=True)
+    for pg in (16, 64):
+        gpu, ref, _ = run_prefill("swa", window, pg, hq, hkv, [0, 37, 300, 1000], [700, 333, 64, 900],
+                                  (305, hq, window, pg))
+        assert_close(gpu, ref, f"prefill W={window} hq={hq} hkv={hkv} PG={pg}")
