@@ -4,15 +4,18 @@
 // prefill is bound by moving q, o and the chunk's K/V rather than by the
 // matrix cores. A workgroup that serves one tile of positions has to stage the
 // whole window (W + positions - 1 keys) for that tile alone, so every key is
-// staged about W / positions times. Here one workgroup (8 waves) walks a run
-// of consecutive tiles of one (sequence, KV head) pair instead: tile t holds
-// 256 query rows (a row = a (position, query head) pair of the KV head's GQA
-// group, so 256 / G positions), the window's 32-key chunks stay in an LDS ring
-// of eight, and each tile stages only the chunk its last positions add. The
-// chunk a tile will need next is loaded into registers while the tile
-// computes; each wave loads its next tile's queries as soon as its last QK^T
-// of the tile has read the current ones; waves run through a tile's chunks
-// without barriers (one barrier per tile).
+// staged about W / positions times. Here one workgroup (16 waves of 16 rows)
+// walks a run of consecutive tiles of one (sequence, KV head) pair instead:
+// tile t holds 256 query rows (a row = a (position, query head) pair of the KV
+// head's GQA group, so 256 / G positions), the window's 32-key chunks stay in
+// an LDS ring of eight, and each tile stages only the chunk its last positions
+// add. The chunk a tile will need next is loaded into registers while the tile
+// computes (waves 0-7 carry its V, waves 8-15 its K); each wave loads its
+// next tile's queries as soon as its last QK^T of the tile has read the
+// current ones; waves run through a tile's chunks without barriers (one
+// barrier per tile). Tiles whose positions all exist issue their loads and
+// stores unconditionally, so the memory counters stay exact along the loop
+// and no wait covers more than the operation it is for.
 //
 // Used when G >= 8 and W + 256 / G - 1 <= 160: a tile then spans at most 7
 // chunks and the next tile adds at most one, so the ring of 8 is never short.
@@ -29,6 +32,7 @@
 // staged as zeros and every column masks its own window.
 #include <algorithm>
 #include <cfloat>
+#include <type_traits>
 
 #include "hswa_common.h"
 #include "hswa_launch.h"
@@ -36,24 +40,24 @@
 namespace hswa {
 namespace {
 
-constexpr int kRThreads = 512;
-constexpr int kRRows = 256;                      // query rows per tile (8 waves x 32)
+constexpr int kRThreads = 1024;
+constexpr int kRRows = 256;                      // query rows per tile (16 waves x 16)
 constexpr int kRChunk = 32;                      // keys per chunk
 constexpr int kRBufs = 8;                        // LDS ring of chunks
 constexpr int kRKBytes = kRChunk * kHeadDim * 2; // 8 KiB of K per chunk
 constexpr int kRBufBytes = 2 * kRKBytes;         // K, then V^T
-constexpr int kRCG = 2;                          // 16-column MFMA groups per wave
+constexpr int kRCG = 1;                          // 16-column MFMA groups per wave
 constexpr float kRLaneSumLimit = 4096.f;         // lane share of a row sum that raises the maximum
 constexpr int kRTargetGroups = 256;              // workgroups a launch aims for (one per CU)
 
-// Staging registers of one chunk: waves 0-3 carry its V (two 16-byte pieces a
-// thread), waves 4-7 its K (two pieces a thread).
+// Staging registers of one chunk: waves 0-7 carry its V, waves 8-15 its K,
+// one 16-byte piece a thread.
 struct RStage {
-  u32x4 a[2];
-  uint32_t keep;  // K: bit i = piece i holds data; V: bits 8 i .. 8 i + 7 = its keys that do
+  u32x4 a;
+  uint32_t keep;  // K: bit 0 = the piece holds data; V: bits 0 .. 7 = its keys that do
 };
 
-__global__ __launch_bounds__(kRThreads) __attribute__((amdgpu_waves_per_eu(2))) void prefill_run_kernel(
+__global__ __launch_bounds__(kRThreads) __attribute__((amdgpu_waves_per_eu(4))) void prefill_run_kernel(
     PrefillParams p) {
   __shared__ __attribute__((aligned(16))) unsigned char s_lds[kRBufs * kRBufBytes];
 
@@ -125,53 +129,49 @@ __global__ __launch_bounds__(kRThreads) __attribute__((amdgpu_waves_per_eu(2))) 
   auto v_dim = [](int idx) { return (idx >> 6) * 16 + (idx & 15); };
   auto v_keys = [](int idx) { return ((idx >> 4) & 3) * 8; };
   const u32x4 zero = {0u, 0u, 0u, 0u};
-  const bool vwave = wave < 4;          // waves 0-3 stage V, waves 4-7 stage K
-  const int st_tid = tid & 255;         // thread index within its half
+  const bool vwave = wave < 8;   // waves 0-7 stage V, waves 8-15 stage K
+  const int sidx = tid & 511;    // the piece this thread stages
   auto fetch = [&](int c, RStage &st) {
     c = min(c, nch - 1);  // past the end: a repeat of the last chunk, never stored
     const int kb = chunk_base(c);
     const bool cached = c < ncached;
-    const uint16_t *src[2];
-    uint32_t keep = 0u;
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int idx = st_tid + 256 * i;
-      if (vwave) {
-        if (cached) {
-          const int j0 = kb + v_keys(idx);
-          const int page = page_at(j0);
-          src[i] = pv.v_pool + v_offset(pv, page >= 0 ? page : 0, hkv, g, j0 & (pg - 1), v_dim(idx));
-          keep |= (page >= 0 ? key_range_bits(j0, klo, chi) : 0u) << (8 * i);
-        } else {
-          // a row piece: key 8 wave + 4 i + lane / 16, dims 8 (lane % 16) .. +7
-          const int jv = kb + 8 * wave + 4 * i + (lane >> 4);
-          const bool in = jv >= klo && jv <= khi;
-          src[i] = p.v_new + ((int64_t)(tok0 + (in ? jv - P : 0)) * hkv + g) * kHeadDim + (lane & 15) * 8;
-          keep |= (in ? 0xFFu : 0u) << (8 * i);
-        }
+    const uint16_t *src;
+    uint32_t keep;
+    if (vwave) {
+      if (cached) {
+        const int j0 = kb + v_keys(sidx);
+        const int page = page_at(j0);
+        src = pv.v_pool + v_offset(pv, page >= 0 ? page : 0, hkv, g, j0 & (pg - 1), v_dim(sidx));
+        keep = page >= 0 ? key_range_bits(j0, klo, chi) : 0u;
       } else {
-        const int j = kb + k_key(idx);
-        if (cached) {
-          const int page = page_at(j);
-          const bool in = j >= klo && j <= chi && page >= 0;
-          src[i] = pv.k_pool + k_offset(pv, in ? page : 0, hkv, g, j & (pg - 1), k_dim(idx));
-          keep |= (in ? 1u : 0u) << i;
-        } else {
-          const bool in = j >= klo && j <= khi;
-          src[i] = p.k_new + ((int64_t)(tok0 + (in ? j - P : 0)) * hkv + g) * kHeadDim + k_dim(idx);
-          keep |= (in ? 1u : 0u) << i;
-        }
+        // a row piece: key 4 wave + lane / 16, dims 8 (lane % 16) .. +7
+        const int jv = kb + 4 * wave + (lane >> 4);
+        const bool in = jv >= klo && jv <= khi;
+        src = p.v_new + ((int64_t)(tok0 + (in ? jv - P : 0)) * hkv + g) * kHeadDim + (lane & 15) * 8;
+        keep = in ? 0xFFu : 0u;
+      }
+    } else {
+      const int j = kb + k_key(sidx);
+      if (cached) {
+        const int page = page_at(j);
+        const bool in = j >= klo && j <= chi && page >= 0;
+        src = pv.k_pool + k_offset(pv, in ? page : 0, hkv, g, j & (pg - 1), k_dim(sidx));
+        keep = in ? 1u : 0u;
+      } else {
+        const bool in = j >= klo && j <= khi;
+        src = p.k_new + ((int64_t)(tok0 + (in ? j - P : 0)) * hkv + g) * kHeadDim + k_dim(sidx);
+        keep = in ? 1u : 0u;
       }
     }
-#pragma unroll
-    for (int i = 0; i < 2; ++i) st.a[i] = ldg128_global(src[i]);
+    st.a = ldg128_global(src);
     st.keep = keep;
   };
   auto lds128 = [&](uint32_t off) { return reinterpret_cast<u32x4 *>(s_lds + off); };
   auto buf_off = [&](int buf) { return (uint32_t)__builtin_amdgcn_readfirstlane(buf * kRBufBytes); };
-  // V^T bytes of dims 8 (lane % 16) + 2 (lane / 16) and + 1, keys 8 wave .. +7
-  const uint32_t st_vrow = kRKBytes + ((((8 * (lane & 15)) >> 4) * 64 + ((8 * (lane & 15) + 2 * (lane >> 4)) & 15) +
-                                        16 * (wave & 3)) * 16);
+  // V^T byte of dim d = 8 (lane % 16) + 2 (lane / 16), keys 4 wave .. +3: the
+  // 16-byte piece of key group wave / 2, its half wave % 2
+  const int vd = 8 * (lane & 15) + 2 * (lane >> 4);
+  const uint32_t st_vrow = kRKBytes + (((vd >> 4) * 64 + (vd & 15) + 16 * (wave >> 1)) * 16) + 8 * (wave & 1);
   // 4 x 4 transpose of dwords across the lanes l, l ^ 16, l ^ 32, l ^ 48.
   auto transpose4 = [&](const u32x4 &t, uint32_t (&w)[4]) {
     const auto a = __builtin_amdgcn_permlane32_swap(t[0], t[2], false, false);
@@ -183,40 +183,27 @@ __global__ __launch_bounds__(kRThreads) __attribute__((amdgpu_waves_per_eu(2))) 
     w[2] = (uint32_t)d[0];
     w[3] = (uint32_t)d[1];
   };
-  auto store = [&](int c, const RStage &st0) {
+  auto store = [&](int c, const RStage &st) {
     const bool cached = c < ncached;
     const uint32_t bo = buf_off(c % kRBufs);
-    RStage st = st0;
     if (!vwave) {
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        st.a[i] = (st.keep >> i) & 1u ? st.a[i] : zero;
-        *lds128(bo + 16 * (st_tid + 256 * i)) = st.a[i];
-      }
+      *lds128(bo + 16 * sidx) = st.keep & 1u ? st.a : zero;
     } else if (cached) {
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const uint32_t k8 = (st.keep >> (8 * i)) & 0xFFu;
-        if (k8 != 0xFFu) st.a[i] = keep_bf16x8(st.a[i], k8);
-        *lds128(bo + kRKBytes + 16 * (st_tid + 256 * i)) = st.a[i];
-      }
+      const uint32_t k8 = st.keep & 0xFFu;
+      *lds128(bo + kRKBytes + 16 * sidx) = k8 != 0xFFu ? keep_bf16x8(st.a, k8) : st.a;
     } else {
-      // lanes l % 16 + 16 m hold keys 8 wave + 4 i + m (piece i) x dims
-      // 8 (l % 16) .. +7; after the transposes lane m holds dims 2 m, 2 m + 1 of
-      // keys 8 wave .. +7, split into one V^T piece per dim
-#pragma unroll
-      for (int i = 0; i < 2; ++i) st.a[i] = (st.keep >> (8 * i)) & 1u ? st.a[i] : zero;
-      uint32_t w[8];
-      transpose4(st.a[0], *reinterpret_cast<uint32_t(*)[4]>(&w[0]));
-      transpose4(st.a[1], *reinterpret_cast<uint32_t(*)[4]>(&w[4]));
-      u32x4 lo, hi;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        lo[j] = __builtin_amdgcn_perm(w[2 * j + 1], w[2 * j], 0x05040100u);
-        hi[j] = __builtin_amdgcn_perm(w[2 * j + 1], w[2 * j], 0x07060302u);
-      }
-      *lds128(bo + st_vrow) = lo;
-      *lds128(bo + st_vrow + 16) = hi;
+      // lanes l % 16 + 16 m hold key 4 wave + m x dims 8 (l % 16) .. +7; after
+      // the transpose lane m holds dims 2 m, 2 m + 1 of keys 4 wave .. +3,
+      // packed into half a V^T piece per dim
+      uint32_t w[4];
+      transpose4(st.keep & 1u ? st.a : zero, w);
+      u32x2 lo, hi;
+      lo[0] = __builtin_amdgcn_perm(w[1], w[0], 0x05040100u);
+      lo[1] = __builtin_amdgcn_perm(w[3], w[2], 0x05040100u);
+      hi[0] = __builtin_amdgcn_perm(w[1], w[0], 0x07060302u);
+      hi[1] = __builtin_amdgcn_perm(w[3], w[2], 0x07060302u);
+      *reinterpret_cast<u32x2 *>(s_lds + bo + st_vrow) = lo;
+      *reinterpret_cast<u32x2 *>(s_lds + bo + st_vrow + 16) = hi;
     }
   };
 
@@ -263,9 +250,6 @@ __global__ __launch_bounds__(kRThreads) __attribute__((amdgpu_waves_per_eu(2))) 
       }
     }
     if (prefetch) load_q(tnext);
-    u32x4 vf[8];
-#pragma unroll
-    for (int dt = 0; dt < 8; ++dt) vf[dt] = *lds128(a + kRKBytes + 1024 * dt);
     if (!(kb >= wint_lo && kb + kRChunk - 1 <= min(wint_hi, kend))) {
       const int j0 = kb + 8 * q;  // this lane's keys are kb + 8 q + e, e = 4 ab + i
 #pragma unroll
@@ -320,10 +304,18 @@ __global__ __launch_bounds__(kRThreads) __attribute__((amdgpu_waves_per_eu(2))) 
     }
 #pragma unroll
     for (int cg = 0; cg < kRCG; ++cg) lsum[cg] += ts[cg];
+    // V^T operands in two batches of four (fewer registers live at once)
 #pragma unroll
-    for (int dt = 0; dt < 8; ++dt)
+    for (int h = 0; h < 2; ++h) {
+      u32x4 vf[4];
 #pragma unroll
-      for (int cg = 0; cg < kRCG; ++cg) acc[cg][dt] = mfma16x16x32(vf[dt], pf[cg], acc[cg][dt]);
+      for (int d4 = 0; d4 < 4; ++d4) vf[d4] = *lds128(a + kRKBytes + 1024 * (4 * h + d4));
+#pragma unroll
+      for (int d4 = 0; d4 < 4; ++d4)
+#pragma unroll
+        for (int cg = 0; cg < kRCG; ++cg)
+          acc[cg][4 * h + d4] = mfma16x16x32(vf[d4], pf[cg], acc[cg][4 * h + d4]);
+    }
   };
 
   // ---- warm-up: the chunks of the first tile, two stages in flight ----
@@ -337,10 +329,21 @@ __global__ __launch_bounds__(kRThreads) __attribute__((amdgpu_waves_per_eu(2))) 
     if (c + 1 <= ce0) store(c + 1, sb);
   }
   int stored = ce0 + 1;  // next chunk to store
-  fetch(stored, sa);     // the chunk the next tile adds
   load_q(t0);
+  fetch(stored, sa);     // the chunk the next tile adds
+  // Everything issued so far completes here, once: the tile loop then starts
+  // with nothing pending, and the wait for each tile's queries counts only
+  // the operations the previous tile issued after them (the next stage's
+  // loads and the output stores), instead of waiting for those as well.
+  __builtin_amdgcn_s_waitcnt(0);
 
-  for (int t = t0; t < t1; ++t) {
+  // One tile. kFull: every row of the tile is a valid position (all tiles but
+  // a sequence's last); then every memory operation of the tile is issued
+  // unconditionally, so the wait before the staged chunk's LDS store counts
+  // exactly the operations issued after its loads and never waits for the
+  // query prefetch or the output stores.
+  auto tile = [&](int t, auto full_tag) {
+    constexpr bool kFull = decltype(full_tag)::value;
     const int q0 = t * npos, q1 = min(C, q0 + npos) - 1;
     __syncthreads();
 #pragma unroll
@@ -355,11 +358,12 @@ __global__ __launch_bounds__(kRThreads) __attribute__((amdgpu_waves_per_eu(2))) 
 #pragma unroll
       for (int dt = 0; dt < 8; ++dt) acc[cg][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    // this wave's rows: positions po_lo .. po_hi of the tile
+    // this wave's rows: positions po_lo .. po_hi of the tile (a wave has no
+    // rows only in a sequence's last, partial tile, which ends its run)
     const int po_lo = (wave * 16 * kRCG) / G;
     const int po_hi = min((wave * 16 * kRCG + 16 * kRCG - 1) / G, q1 - q0);
     const bool more = t + 1 < t1;
-    if (po_lo <= q1 - q0) {
+    if (kFull || po_lo <= q1 - q0) {
       const int wklo = max(0, P + q0 + po_lo - W + 1), wkhi = P + q0 + po_hi;
       const int wint_lo = max(0, P + q0 + po_hi - W + 1), wint_hi = P + q0 + po_lo;
       const int cw0 = chunk_of(wklo), cw1 = chunk_of(wkhi);
@@ -370,8 +374,6 @@ __global__ __launch_bounds__(kRThreads) __attribute__((amdgpu_waves_per_eu(2))) 
         chunk(c, chunk_base(c), c < ncached ? chi : khi, wint_lo, wint_hi, c == cw0, false, 0);
       chunk(cw1, chunk_base(cw1), cw1 < ncached ? chi : khi, wint_lo, wint_hi, cw1 == cw0, true,
             more ? t + 1 : t);
-    } else if (more) {
-      load_q(t + 1);
     }
     // normalise this tile's rows
     u32x2 wo[kRCG][8];
@@ -386,29 +388,32 @@ __global__ __launch_bounds__(kRThreads) __attribute__((amdgpu_waves_per_eu(2))) 
       }
     }
     // Stage the chunk the next tile adds now, before this tile's output stores
-    // (its loads went out a tile ago; a wait for them then never waits for the
-    // stores). Its buffer held a chunk that ends before this tile's range, so
-    // waves still computing this tile are not disturbed; the barrier that
-    // opens the next tile makes it visible.
-    if (more) {
-      const int ce_next = chunk_of(tile_last_key(t + 1));
-      while (stored <= ce_next) {
-        store(stored, sa);
-        ++stored;
-        fetch(stored, sa);
-      }
-    }
+    // (its loads went out a tile ago). A tile's last key is its last query's
+    // position, always a new key, and the next tile's lies at most 32
+    // positions further (256 / G <= 32), so it adds at most one chunk. Its
+    // buffer held a chunk that ends before this tile's range, so waves still
+    // computing this tile are not disturbed; the barrier that opens the next
+    // tile makes it visible. The stage is reloaded either way (with the same
+    // chunk when nothing was stored), keeping the loads unconditional.
+    const bool adv = more && stored <= chunk_of(tile_last_key(t + 1));
+    if (adv) store(stored, sa);
+    stored += adv ? 1 : 0;
+    fetch(stored, sa);
     // write this tile's rows
 #pragma unroll
     for (int cg = 0; cg < kRCG; ++cg) {
-      if (!cval[cg]) continue;
+      if (!kFull && !cval[cg]) continue;
       const int row = wave * (16 * kRCG) + cg * 16 + r;
       const int po = row / G, head = row - po * G;
       uint16_t *orow = p.out + ((int64_t)(tok0 + q0 + po) * hq + (int64_t)g * G + head) * kHeadDim;
 #pragma unroll
       for (int dt = 0; dt < 8; ++dt) *reinterpret_cast<u32x2 *>(orow + 16 * dt + 4 * q) = wo[cg][dt];
     }
-  }
+  };
+  const int tfull = min(t1, C / npos);  // tiles before tfull hold npos valid positions
+  int t = t0;
+  for (; t < tfull; ++t) tile(t, std::true_type{});
+  for (; t < t1; ++t) tile(t, std::false_type{});
 }
 
 }  // namespace
