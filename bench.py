@@ -7,8 +7,9 @@ Headline workload (the largest configuration that fits one GPU): a 70-layer
 hybrid decode step, 60 SWA layers (W = 128) and 10 FULL layers (FULL iff
 layer % 7 == 6), 16 sequences at a 131072-token cached context, 64 query / 8 KV
 heads, head dim 128, bf16, page size 64, pages placed by a seeded permutation.
-One step appends one new token per sequence to every layer (hswa_kv_append)
-and decodes it (hswa_decode). Every layer's pools hold their own synthetic KV
+One step stores one new token per sequence in every layer and decodes it
+(hswa_decode_append: one launch for an SWA layer, the append kernel then the
+split decode for a FULL layer). Every layer's pools hold their own synthetic KV
 (86 GB of FULL pages, 12 MiB per SWA layer), resident in HBM before the timed
 region. value = algorithmic decode bytes of the step (K and V of every visible
 key read once per (sequence, KV head, layer), plus q and o) / step time.
@@ -315,11 +316,17 @@ class Stack70Bench:
 
         hswa.decode(L["layer"], self.shape, L["kv"].cache, L["q"], self.lens, self.maxc, L["out"], workspace=self.ws)
 
+    def step_layer(self, L):
+        """One layer's step: store the new token and decode it (one call)."""
+        from paper_2607_13095_amd import hswa
+
+        hswa.decode_append(L["layer"], self.shape, L["kv"].cache, L["q"], L["k_new"], L["v_new"], self.lens,
+                           self.maxc, L["out"], workspace=self.ws)
+
     def run(self, kinds=("full", "swa")):
         for L in self.layers:
             if L["kind"] in kinds:
-                self.append(L)
-                self.decode(L)
+                self.step_layer(L)
 
     def graph(self, kinds):
         """The step (or one kind's layers) captured as one HIP graph."""
@@ -444,8 +451,12 @@ class DecodeBench:
         from paper_2607_13095_amd import hswa
 
         for L in self.layers:
-            hswa.kv_append(L["layer"], self.shape, L["kv"].cache, L["k_new"], L["v_new"], self.cu1, self.start)
-            self.decode(L)
+            if self.nq == 1:  # store the new token and decode it in one call
+                hswa.decode_append(L["layer"], self.shape, L["kv"].cache, L["q"], L["k_new"], L["v_new"],
+                                   self.ctx_lens, self.maxc, L["out"], workspace=L["ws"])
+            else:
+                hswa.kv_append(L["layer"], self.shape, L["kv"].cache, L["k_new"], L["v_new"], self.cu1, self.start)
+                self.decode(L)
 
     def decode(self, L):
         from paper_2607_13095_amd import hswa
@@ -984,6 +995,8 @@ def headline(args, flush):
         rep["full_decode_call"] = time_calls(lambda: st.decode(Lf), flush, reps=10)
         rep["swa_decode_call"] = time_calls(lambda: st.decode(Ls), flush)
         rep["swa_decode_call_back_to_back_ms"] = round(time_back_to_back(lambda: st.decode(Ls), 50), 5)
+        rep["swa_step_call"] = time_calls(lambda: st.step_layer(Ls), flush)
+        rep["swa_step_call_back_to_back_ms"] = round(time_back_to_back(lambda: st.step_layer(Ls), 50), 5)
         full_ms = time_back_to_back(lambda: st.run(("full",)), 3)
         swa_ms = time_back_to_back(lambda: st.run(("swa",)), 10)
         g_step = st.graph(("full", "swa"))

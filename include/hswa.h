@@ -21,13 +21,14 @@
  * ---------------------------------------------------------------------------
  * Conventions shared by every call
  * ---------------------------------------------------------------------------
- * Ownership. The caller owns every buffer. The library never allocates, frees
- *   or keeps device memory, and keeps one piece of state
- *   between calls: per device, the number of waves the FULL decode kernel can
- *   hold resident, looked up on the first FULL decode call on that device and
- *   cached (atomically) for the life of the process. All calls are
- *   thread-safe. Pointers marked "device" are device (HBM) addresses, "host"
- *   pointers are read synchronously during the call.
+ * Ownership. The caller owns every buffer. The library never allocates or
+ *   frees device memory. It keeps two pieces of state between calls: per
+ *   device, the number of waves the FULL decode kernel can hold resident,
+ *   looked up on the first FULL decode call on that device and cached
+ *   (atomically) for the life of the process; and the fixed device array of
+ *   hswa_decode_noalloc (a static array of the library, one per device).
+ *   All calls are thread-safe. Pointers marked "device" are device (HBM)
+ *   addresses, "host" pointers are read synchronously during the call.
  * Streams. Compute calls enqueue on `stream` (a hipStream_t passed as void*;
  *   NULL = the default stream) and return without synchronising. Argument
  *   validation is synchronous and returns a status; a failed launch returns
@@ -71,7 +72,8 @@
  *   entries per sequence.
  * Ordering. Decode: hswa_kv_append of the new token, then hswa_decode (which
  *   reads the new token from the cache; the ring slot the new token at c
- *   overwrites held position c - R*PG, outside the window since R*PG > W).
+ *   overwrites held position c - R*PG, outside the window since R*PG > W);
+ *   or both at once with hswa_decode_append.
  *   Prefill:
  *   hswa_prefill first (the chunk's own keys come from k_new / v_new), then
  *   hswa_kv_append of the chunk. For SWA this order is required: a chunk
@@ -236,6 +238,25 @@ hswa_status hswa_decode(hswa_layer layer, const hswa_shape *shape, const hswa_ca
                         const void *q, const int32_t *context_lens, int32_t ns,
                         int32_t max_context_len, void *workspace, size_t workspace_bytes,
                         void *out, void *stream);
+
+/* One decode step of a layer, append included ("KVCache Storage Analysis":
+ * an SWA layer's decode reads only its window, so its cost is a short chain of
+ * dependent loads and a launch; "KVCache Dual-Pool Design": the step's token
+ * goes to its pool slot, the ring overwrite evicting the oldest position).
+ * For every sequence b with c_b = min(context_lens[b], max_context_len) >= 1:
+ * stores k_new[b] / v_new[b] at position c_b - 1 exactly as hswa_kv_append
+ * with cu_seqlens = 0, 1, .., ns and start_pos[b] = c_b - 1 would, and writes
+ * out[b] as hswa_decode with the same context_lens would after that append.
+ * Sequences with c_b < 1 store nothing and get a zero row. SWA layers, and FULL
+ * layers short enough for one pass, do both in one kernel whose new key comes
+ * from k_new / v_new (results equal the two calls' up to rounding order); other
+ * FULL layers run the append kernel, then the decode kernels.
+ * k_new, v_new: device bf16 [ns][Hkv][D]; the other arguments as hswa_decode.
+ * The call must not overlap another call writing the same layer's pools. */
+hswa_status hswa_decode_append(hswa_layer layer, const hswa_shape *shape, const hswa_cache *cache,
+                               const void *q, const void *k_new, const void *v_new,
+                               const int32_t *context_lens, int32_t ns, int32_t max_context_len,
+                               void *workspace, size_t workspace_bytes, void *out, void *stream);
 
 /* Bytes of the fixed device array behind hswa_decode_noalloc. */
 #define HSWA_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)

@@ -20,7 +20,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libhswa.so")
-SOURCES = ["api.hip", "kv_append.hip", "decode.hip", "prefill.hip", "prefill_window.hip", "prefill_run.hip", "noalloc.hip"]
+SOURCES = ["api.hip", "kv_append.hip", "decode.hip", "prefill.hip", "prefill_window.hip", "prefill_run.hip", "noalloc.hip", "decode_append.hip"]
 HOST_SOURCES = ["allocator.cpp", "prefix_tree.cpp"]
 CXX = os.environ.get("CXX", shutil.which("g++") or "g++")
 CXXFLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-I", os.path.join(ROOT, "include")]

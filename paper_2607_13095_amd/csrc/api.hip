@@ -231,9 +231,12 @@ namespace {
 
 // Shared body of the decode entry points. With `noalloc` the FULL split
 // partials go to the library's fixed device array instead of `workspace`.
+// With k_new / v_new (one query per sequence) the call first stores the step's
+// new token of every sequence, in the same launch when the kernel allows it.
 hswa_status decode_impl(hswa_layer layer, const hswa_shape *shape, const hswa_cache *cache, const void *q,
                         const int32_t *context_lens, int32_t ns, int32_t num_queries, int32_t max_context_len,
-                        void *workspace, size_t workspace_bytes, bool noalloc, void *out, void *stream) {
+                        void *workspace, size_t workspace_bytes, bool noalloc, void *out, void *stream,
+                        const void *k_new = nullptr, const void *v_new = nullptr, bool append = false) {
   hswa_status st;
   if ((st = check_layer(layer)) != HSWA_OK) return st;
   if ((st = check_shape(shape)) != HSWA_OK) return st;
@@ -247,6 +250,7 @@ hswa_status decode_impl(hswa_layer layer, const hswa_shape *shape, const hswa_ca
     return HSWA_ERR_CAPACITY;
   if (ns == 0) return HSWA_OK;
   if (!q || !context_lens || !out) return HSWA_ERR_INVALID_ARG;
+  if (append && (!k_new || !v_new)) return HSWA_ERR_INVALID_ARG;
   hswa::DecodeParams p{};
   p.pool = pv;
   p.q = static_cast<const uint16_t *>(q);
@@ -279,6 +283,22 @@ hswa_status decode_impl(hswa_layer layer, const hswa_shape *shape, const hswa_ca
     p.max_splits = 1;
   }
   hipStream_t s = static_cast<hipStream_t>(stream);
+  if (append) {
+    p.k_new = static_cast<const uint16_t *>(k_new);
+    p.v_new = static_cast<const uint16_t *>(v_new);
+    if (hswa::decode_append_fused(p)) return finish_launch(hswa::launch_decode_append(p, s), s);
+    hswa::AppendParams a{};
+    a.pool = pv;
+    a.k_new = p.k_new;
+    a.v_new = p.v_new;
+    a.ns = ns;
+    a.total_tokens = ns;
+    a.hkv = p.hkv;
+    a.ctx_lens = context_lens;
+    a.max_ctx = max_context_len;
+    const hipError_t e = hswa::launch_kv_append(a, s);
+    if (e != hipSuccess) return HSWA_ERR_LAUNCH;
+  }
   return finish_launch(hswa::launch_decode(p, s), s);
 }
 
@@ -298,6 +318,14 @@ hswa_status hswa_decode(hswa_layer layer, const hswa_shape *shape, const hswa_ca
                         size_t workspace_bytes, void *out, void *stream) {
   return decode_impl(layer, shape, cache, q, context_lens, ns, 1, max_context_len, workspace, workspace_bytes, false,
                      out, stream);
+}
+
+hswa_status hswa_decode_append(hswa_layer layer, const hswa_shape *shape, const hswa_cache *cache, const void *q,
+                               const void *k_new, const void *v_new, const int32_t *context_lens, int32_t ns,
+                               int32_t max_context_len, void *workspace, size_t workspace_bytes, void *out,
+                               void *stream) {
+  return decode_impl(layer, shape, cache, q, context_lens, ns, 1, max_context_len, workspace, workspace_bytes, false,
+                     out, stream, k_new, v_new, true);
 }
 
 hswa_status hswa_decode_noalloc(hswa_layer layer, const hswa_shape *shape, const hswa_cache *cache, const void *q,

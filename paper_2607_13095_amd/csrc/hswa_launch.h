@@ -38,6 +38,11 @@ struct AppendParams {
   const int32_t *start_pos;
   int64_t *slot_out;      // [T] or null
   int32_t ns, total_tokens, hkv;
+  // Decode-step mode (ctx_lens non-null): token b is sequence b's, at position
+  // min(ctx_lens[b], max_ctx) - 1 (none if that is negative); cu_seqlens and
+  // start_pos are not read.
+  const int32_t *ctx_lens;
+  int32_t max_ctx;
 };
 
 struct DecodeParams {
@@ -54,6 +59,8 @@ struct DecodeParams {
   int32_t span_waves;     // FULL split: waves the chunk order is divided over (set at launch)
   int32_t item_cols;      // (query, head) columns of one item (set at launch)
   float scale_log2;       // scale * log2(e)
+  const uint16_t *k_new;  // decode step: the new token's K / V rows [ns][Hkv][D]
+  const uint16_t *v_new;
 };
 
 struct PrefillParams {
@@ -70,6 +77,10 @@ struct PrefillParams {
 
 hipError_t launch_kv_append(const AppendParams &p, hipStream_t stream);
 hipError_t launch_decode(const DecodeParams &p, hipStream_t stream);
+// Decode step with its append in the same launch (decode_append.hip): one
+// query per sequence, whole-range items of at most 8 chunks, PG >= 32.
+bool decode_append_fused(const DecodeParams &p);
+hipError_t launch_decode_append(const DecodeParams &p, hipStream_t stream);
 hipError_t launch_prefill(const PrefillParams &p, hipStream_t stream);
 // SWA prefill whose window is at most kPrefillWindowMax keys: 128 query rows
 // per workgroup over the window's keys only (prefill_window.hip).

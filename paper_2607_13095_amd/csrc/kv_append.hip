@@ -34,11 +34,19 @@ __device__ int find_seq(const int32_t *cu, int ns, int t) {
 }
 
 __device__ int64_t slot_of_token(const AppendParams &p, const int32_t *cu, int t) {
-  const int b = find_seq(cu, p.ns, t);
-  if (b < 0) return -1;
-  const int64_t start = p.start_pos[b];
-  const int64_t j = start + (t - cu[b]);
-  const int64_t len_after = start + (cu[b + 1] - cu[b]);
+  int b;
+  int64_t j, len_after;
+  if (p.ctx_lens) {  // decode step: token t is sequence t's
+    b = t;
+    len_after = min(p.ctx_lens[b], p.max_ctx);
+    j = len_after - 1;
+  } else {
+    b = find_seq(cu, p.ns, t);
+    if (b < 0) return -1;
+    const int64_t start = p.start_pos[b];
+    j = start + (t - cu[b]);
+    len_after = start + (cu[b + 1] - cu[b]);
+  }
   if (j < 0) return -1;
   const PoolView &pv = p.pool;
   const int64_t pg = int64_t(1) << pv.pg_shift;
@@ -64,7 +72,7 @@ __global__ __launch_bounds__(kThreads) void kv_append_kernel(AppendParams p) {
   const int ntok = min(kTokPerBlock, p.total_tokens - t0);
   // One coalesced load of cu_seqlens instead of a chain of dependent loads in
   // the binary search.
-  const bool lds_cu = p.ns <= kLdsSeqs;
+  const bool lds_cu = p.ns <= kLdsSeqs && !p.ctx_lens;
   if (lds_cu) {
     for (int i = tid; i <= p.ns; i += kThreads) s_cu[i] = p.cu_seqlens[i];
   }

@@ -32,7 +32,7 @@ EXPORTS = ["hswa_ring_pages", "hswa_page_bytes", "hswa_build_block_table", "hswa
            "hswa_prefix_tree_create", "hswa_prefix_tree_destroy", "hswa_prefix_tree_insert",
            "hswa_prefix_tree_match", "hswa_prefix_tree_release_swa", "hswa_prefix_tree_evict",
            "hswa_prefix_tree_stats", "hswa_decode_multi_workspace_bytes", "hswa_decode_multi",
-           "hswa_decode_noalloc"]
+           "hswa_decode_noalloc", "hswa_decode_append"]
 
 # bytes of the library's fixed device array behind hswa_decode_noalloc
 NOALLOC_SCRATCH_BYTES = 128 << 20
@@ -95,6 +95,7 @@ def load():
         "hswa_decode_multi_workspace_bytes": (SZ, [SP, I32, I32, I32]),
         "hswa_decode_multi": (ctypes.c_int, [LP, SP, CP, P, P, I32, I32, I32, P, SZ, P, P]),
         "hswa_decode_noalloc": (ctypes.c_int, [LP, SP, CP, P, P, I32, I32, P, P]),
+        "hswa_decode_append": (ctypes.c_int, [LP, SP, CP, P, P, P, P, I32, I32, P, SZ, P, P]),
         "hswa_allocator_create": (ctypes.c_int, [ctypes.POINTER(_AllocConfig), ctypes.POINTER(P)]),
         "hswa_allocator_destroy": (None, [P]),
         "hswa_allocator_admit": (ctypes.c_int, [P, I32, I64, I32]),
@@ -146,7 +147,10 @@ class Layer:
         return cls("swa_paged", window)
 
     def c(self):
-        return _Layer(self._KINDS[self.kind], self.window)
+        key = (self.kind, self.window)
+        if getattr(self, "_ck", None) != key:
+            self._c, self._ck = _Layer(self._KINDS[self.kind], self.window), key
+        return self._c
 
 
 class Shape:
@@ -156,12 +160,14 @@ class Shape:
         self.scale = float(1.0 / np.sqrt(head_dim) if scale is None else scale)
 
     def c(self):
-        return _Shape(self.num_q_heads, self.num_kv_heads, self.head_dim, self.page_size, self.scale)
+        key = (self.num_q_heads, self.num_kv_heads, self.head_dim, self.page_size, self.scale)
+        if getattr(self, "_ck", None) != key:
+            self._c, self._ck = _Shape(*key), key
+        return self._c
 
 
 def _ptr(t, name, dtypes, numel=None):
-    import torch
-
+    torch = _torch()
     if t is None:
         return None
     if not isinstance(t, torch.Tensor):
@@ -177,16 +183,24 @@ def _ptr(t, name, dtypes, numel=None):
     return t.data_ptr()
 
 
-def _bf16():
-    import torch
+_TORCH = None
 
-    return (torch.bfloat16,)
+
+def _torch():
+    global _TORCH
+    if _TORCH is None:
+        import torch
+
+        _TORCH = torch
+    return _TORCH
+
+
+def _bf16():
+    return (_torch().bfloat16,)
 
 
 def _i32():
-    import torch
-
-    return (torch.int32,)
+    return (_torch().int32,)
 
 
 V_BLOCK_MAX = 32
@@ -231,12 +245,19 @@ class Cache:
         self.num_pages, self.stride = int(npg), int(block_table.shape[1])
 
     def c(self):
-        return _Cache(_ptr(self.k_pool, "k_pool", _bf16()), _ptr(self.v_pool, "v_pool", _bf16()), self.num_pages,
-                      _ptr(self.block_table, "block_table", _i32()), self.stride)
+        # the tensors are fixed at construction: the struct is built (and the
+        # tensors checked) once
+        if getattr(self, "_c", None) is None:
+            self._c = _Cache(_ptr(self.k_pool, "k_pool", _bf16()), _ptr(self.v_pool, "v_pool", _bf16()),
+                             self.num_pages, _ptr(self.block_table, "block_table", _i32()), self.stride)
+        return self._c
 
 
 def _check_cache(shape: Shape, cache: Cache, ns: int):
     """The pools and the table must match the shape the kernels are told."""
+    key = (shape.num_kv_heads, shape.page_size, shape.head_dim, ns)
+    if getattr(cache, "_checked", None) == key:
+        return
     v = cache.v_pool.shape
     if int(v[1]) != shape.num_kv_heads:
         raise ValueError(f"pools hold {int(v[1])} KV heads, shape says {shape.num_kv_heads}")
@@ -246,13 +267,16 @@ def _check_cache(shape: Shape, cache: Cache, ns: int):
         raise ValueError(f"pool head dim {int(v[3])} != shape head dim {shape.head_dim}")
     if int(cache.block_table.shape[0]) < ns:
         raise ValueError(f"block table has {int(cache.block_table.shape[0])} rows for {ns} sequences")
+    cache._checked = key
 
 
 def _stream(stream):
-    import torch
-
+    torch = _torch()
     if stream is None:
-        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        try:  # the current stream's handle without building a Stream object
+            return ctypes.c_void_p(torch._C._cuda_getCurrentRawStream(torch._C._cuda_getDevice()))
+        except AttributeError:
+            return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
     if isinstance(stream, int):
         return ctypes.c_void_p(stream)
     return ctypes.c_void_p(stream.cuda_stream)
@@ -305,8 +329,7 @@ def decode_split_len(shape: Shape, ns: int, max_context_len: int) -> int:
 def kv_append(layer: Layer, shape: Shape, cache: Cache, k_new, v_new, cu_seqlens, start_pos,
               slot_mapping_out=None, stream=None):
     """Append k_new / v_new [T, Hkv, D] (bf16) to the pools; see hswa_kv_append."""
-    import torch
-
+    torch = _torch()
     ns = int(cu_seqlens.numel()) - 1
     t = int(k_new.shape[0]) if k_new.dim() else 0
     row = shape.num_kv_heads * shape.head_dim
@@ -345,8 +368,7 @@ def decode_multi_workspace_bytes(shape: Shape, ns: int, num_queries: int, max_co
 def decode_multi(layer: Layer, shape: Shape, cache: Cache, q, context_lens, max_context_len: int, out,
                  workspace=None, stream=None):
     """Multi-query decode; q, out [NS, nq, Hq, D]; see hswa_decode_multi."""
-    import torch
-
+    torch = _torch()
     if q.dim() != 4:
         raise ValueError("q must be [NS, num_queries, Hq, D]")
     ns, nq = int(q.shape[0]), int(q.shape[1])
@@ -370,8 +392,7 @@ def decode_multi(layer: Layer, shape: Shape, cache: Cache, q, context_lens, max_
 def decode(layer: Layer, shape: Shape, cache: Cache, q, context_lens, max_context_len: int, out,
            workspace=None, stream=None):
     """Decode one query per sequence; q, out [NS, Hq, D]; see hswa_decode."""
-    import torch
-
+    torch = _torch()
     ns = int(context_lens.numel())
     qrow = shape.num_q_heads * shape.head_dim
     qp = _ptr(q, "q", _bf16(), ns * qrow)
@@ -386,6 +407,30 @@ def decode(layer: Layer, shape: Shape, cache: Cache, q, context_lens, max_contex
     st = load().hswa_decode(layer.c(), ctypes.byref(sh), ctypes.byref(ca), qp, cp, ns, int(max_context_len), wp,
                             wbytes, o, _stream(stream))
     _check(st, "hswa_decode")
+
+
+def decode_append(layer: Layer, shape: Shape, cache: Cache, q, k_new, v_new, context_lens, max_context_len: int,
+                  out, workspace=None, stream=None):
+    """One decode step: store every sequence's new token (k_new / v_new
+    [NS, Hkv, D]) at position context_lens[b] - 1, then decode q [NS, Hq, D]
+    there; see hswa_decode_append."""
+    torch = _torch()
+    ns = int(context_lens.numel())
+    qrow, krow = shape.num_q_heads * shape.head_dim, shape.num_kv_heads * shape.head_dim
+    qp = _ptr(q, "q", _bf16(), ns * qrow)
+    kp = _ptr(k_new, "k_new", _bf16(), ns * krow)
+    vp = _ptr(v_new, "v_new", _bf16(), ns * krow)
+    cp = _ptr(context_lens, "context_lens", _i32(), ns)
+    o = _ptr(out, "out", _bf16(), ns * qrow)
+    wp, wbytes = None, 0
+    if workspace is not None:
+        wp = _ptr(workspace, "workspace", (torch.uint8, torch.float32, torch.int32))
+        wbytes = workspace.numel() * workspace.element_size()
+    _check_cache(shape, cache, ns)
+    sh, ca = shape.c(), cache.c()
+    st = load().hswa_decode_append(layer.c(), ctypes.byref(sh), ctypes.byref(ca), qp, kp, vp, cp, ns,
+                                   int(max_context_len), wp, wbytes, o, _stream(stream))
+    _check(st, "hswa_decode_append")
 
 
 def decode_noalloc(layer: Layer, shape: Shape, cache: Cache, q, context_lens, max_context_len: int, out,

@@ -236,3 +236,23 @@ def test_decode_noalloc_validation():
     assert call(FULL, _cache(stride=1), 2, 100) == -3                 # table too short, as hswa_decode
     assert call(hswa._Layer(1, 0), _cache(), 2, 100) == -1            # SWA window < 1
     assert call(SWA128, _cache(stride=3), 2, 100, q=None) == -1
+
+
+def test_decode_append_validation():
+    """The fused decode step validates like hswa_decode and also needs the new
+    token's K and V rows; every failure returns before any device work."""
+    lib = hswa.load()
+    sh = _shape()
+
+    def call(layer, cache, ns, maxc, q=FAKE, k=FAKE, v=FAKE, ws=None, wsb=0):
+        return lib.hswa_decode_append(layer, ctypes.byref(sh), ctypes.byref(cache), q, k, v, FAKE, ns, maxc, ws, wsb,
+                                      FAKE, None)
+
+    assert call(SWA128, _cache(stride=3), 2, 100, k=None) == -1
+    assert call(SWA128, _cache(stride=3), 2, 100, v=None) == -1
+    assert call(SWA128, _cache(stride=3), 2, 100, q=None) == -1
+    assert call(SWA128, _cache(stride=2), 2, 100) == -3               # ring needs 3 entries (PG 64)
+    assert call(FULL, _cache(stride=1), 2, 100) == -3                 # table too short, as hswa_decode
+    assert call(hswa._Layer(1, 0), _cache(), 2, 100) == -1            # SWA window < 1
+    assert call(FULL, _cache(stride=600), 64, 32769) == -1            # split FULL without a workspace
+    assert call(SWA128, _cache(stride=3), 0, 100) == 0                # nothing to do

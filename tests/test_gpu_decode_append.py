@@ -1,0 +1,169 @@
+"""GPU parity of hswa_decode_append, the decode step with its append fused in.
+
+Every case builds two identical layers holding positions [0, L_b - 1) of
+every sequence. Layer A runs hswa_decode_append for the token at L_b - 1;
+layer B runs hswa_kv_append of that token, then hswa_decode. The checks:
+  * A's output matches the fp64 oracle over the contiguous history;
+  * A's pools equal B's bit for bit (NaN-filled unused slots included), so
+    the fused store is exactly the append;
+  * A's output matches B's within the same tolerance.
+The cases span both kernels behind the call (the fused one for SWA windows
+and short FULL contexts at PG >= 32; the append kernel plus the decode
+kernels for PG 16, windows over 8 chunks and split FULL contexts), windows
+around chunk and page sizes, GQA groups 1 to 32, empty sequences and an
+invalid page under the new token."""
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import attention as OA
+from paper_2607_13095_amd import hswa
+from paper_2607_13095_amd.kvcache import LayerKV, pages_for
+from tests.hswa_testlib import SeqHistory, assert_close, i32, to_bits, to_dev, to_f64
+
+pytestmark = pytest.mark.gpu
+D = 128
+
+
+def _layer(kind, window):
+    return {"swa": hswa.Layer.swa, "swa_paged": hswa.Layer.swa_paged}[kind](window) if kind != "full" \
+        else hswa.Layer.full()
+
+
+def run_step(kind, window, pg, hq, hkv, lens, seed, first=None, table_edit=None):
+    """Returns (A output, B output, oracle, A pools, B pools) for one step."""
+    ns = len(lens)
+    shape = hswa.Shape(hq, hkv, D, pg)
+    layer = _layer(kind, window)
+    final = [max(int(n), 1) for n in lens]
+    npages = pages_for(layer, pg, final) + 2
+    perm = synth.page_permutation(npages, *seed)
+    kvs = [LayerKV(layer, shape, final, perm=perm, extra_pages=2) for _ in range(2)]
+    if table_edit is not None:
+        for kv in kvs:
+            table_edit(kv.block_table)
+    hist = SeqHistory(final, hkv, D, *seed)
+    first = [0] * ns if first is None else list(first)
+    cached = [max(int(n) - 1, 0) for n in lens]
+    kh = np.concatenate([hist.k[b][first[b]:cached[b]] for b in range(ns)])
+    vh = np.concatenate([hist.v[b][first[b]:cached[b]] for b in range(ns)])
+    cu = synth.cu_seqlens([cached[b] - first[b] for b in range(ns)])
+    for kv in kvs:
+        hswa.kv_append(layer, shape, kv.cache, to_dev(kh), to_dev(vh), i32(cu), i32(first))
+    # the step's token of every sequence (not stored where L_b = 0)
+    kn = np.stack([hist.k[b][final[b] - 1] for b in range(ns)])
+    vn = np.stack([hist.v[b][final[b] - 1] for b in range(ns)])
+    qbits = synth.normal_bf16((ns, hq, D), *seed, synth.TAG_QDEC)
+    maxc = max(final)
+    wsb = hswa.decode_workspace_bytes(shape, ns, maxc)
+    ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device="cuda")
+    ctx = i32(lens)
+    out_a = torch.full((ns, hq, D), float("nan"), dtype=torch.bfloat16, device="cuda")
+    out_b = torch.full((ns, hq, D), float("nan"), dtype=torch.bfloat16, device="cuda")
+    q = to_dev(qbits)
+    hswa.decode_append(layer, shape, kvs[0].cache, q, to_dev(kn), to_dev(vn), ctx, maxc, out_a, workspace=ws)
+    has = [1 if n >= 1 else 0 for n in lens]
+    sel = [b for b in range(ns) if has[b]]
+    if sel:
+        hswa.kv_append(layer, shape, kvs[1].cache, to_dev(kn[sel]), to_dev(vn[sel]), i32(synth.cu_seqlens(has)),
+                       i32(cached))
+    hswa.decode(layer, shape, kvs[1].cache, q, ctx, maxc, out_b, workspace=ws)
+    torch.cuda.synchronize()
+    qf = OA.bf16_bits_to_f64(qbits)
+    w = window if kind != "full" else None
+    ref = np.stack([OA.decode(qf[b], OA.bf16_bits_to_f64(hist.k[b]), OA.bf16_bits_to_f64(hist.v[b]), w)
+                    if lens[b] >= 1 else np.zeros((hq, D)) for b in range(ns)])
+    pools = [(to_bits(kv.k_pool), to_bits(kv.v_pool)) for kv in kvs]
+    return to_f64(out_a), to_f64(out_b), ref, pools[0], pools[1]
+
+
+def check(res, what, oracle=True):
+    a, b, ref, pa, pb = res
+    if oracle:
+        assert_close(a, ref, f"{what} vs oracle")
+    assert_close(a, b, f"{what} vs append + decode")
+    assert np.array_equal(pa[0], pb[0]), f"{what}: K pools differ from hswa_kv_append's"
+    assert np.array_equal(pa[1], pb[1]), f"{what}: V pools differ from hswa_kv_append's"
+
+
+def _lens(window, extra=()):
+    base = {0, 1, 2, 31, 32, 33, 63, 64, 65, 200, 1000, 4097}
+    base |= {max(window - 1, 1), window, window + 1, window + 31, window + 32, window + 33}
+    return sorted(base | set(extra))
+
+
+@pytest.mark.parametrize("pg", [16, 32, 64, 128])
+@pytest.mark.parametrize("window", [1, 2, 31, 32, 33, 127, 128, 129, 225, 226])
+def test_decode_append_swa(gpu_lib, pg, window):
+    print(f"[decode-append swa] pg={pg} W={window}", flush=True)
+    check(run_step("swa", window, pg, 64, 8, _lens(window), (300, pg, window)), f"swa W={window} PG={pg}")
+
+
+@pytest.mark.parametrize("hq,hkv", [(8, 8), (8, 1), (16, 1), (32, 1), (32, 2)])
+def test_decode_append_groups(gpu_lib, hq, hkv):
+    print(f"[decode-append groups] hq={hq} hkv={hkv}", flush=True)
+    for kind, window in (("swa", 128), ("swa_paged", 100), ("full", 0)):
+        lens = [0, 5, 129, 250] if kind == "full" else [0, 5, 200, 777, 3000]
+        check(run_step(kind, window, 64, hq, hkv, lens, (301, hq, hkv)), f"{kind} hq={hq} hkv={hkv}")
+
+
+@pytest.mark.parametrize("pg", [32, 64])
+def test_decode_append_full(gpu_lib, pg):
+    """FULL: contexts of at most 256 keys take the fused kernel; a longer
+    batch the split decode after the append kernel."""
+    print(f"[decode-append full] pg={pg}", flush=True)
+    check(run_step("full", 0, pg, 64, 8, [1, 2, 31, 32, 33, 100, 255, 256], (302, pg)), f"full short PG={pg}")
+    check(run_step("full", 0, pg, 64, 8, [1, 257, 1000, 5000, 0], (303, pg)), f"full split PG={pg}")
+
+
+def test_decode_append_swa_paged(gpu_lib):
+    print("[decode-append swa_paged]", flush=True)
+    for window in (1, 64, 128, 200):
+        check(run_step("swa_paged", window, 64, 64, 8, _lens(window), (304, window)), f"swa_paged W={window}")
+
+
+def test_decode_append_invalid_page(gpu_lib):
+    """The new token's page is not a valid page id: nothing is stored and the
+    key is left out, exactly as the two calls do."""
+    print("[decode-append invalid page]", flush=True)
+    lens = [300, 301, 64, 129]
+    pg = 64
+
+    def edit(table):
+        # sequence 0: ring entry of position 299 (logical page 4, entry 4 % 3 = 1)
+        table[0, (299 // pg) % 3] = -1
+        # sequence 2: ring entry of position 63 (logical page 0)
+        table[2, 0] = 1 << 30
+
+    check(run_step("swa", 128, pg, 64, 8, lens, (305,), table_edit=edit), "invalid page", oracle=False)
+
+
+def test_decode_append_stack70_swa_layer(gpu_lib):
+    """The 70-layer step's SWA layer (16 sequences at a 131072-token context,
+    W = 128, PG = 64): every output row against the oracle."""
+    wl = synth.stack70_decode()
+    print(f"[decode-append] {wl.name} SWA layer", flush=True)
+    ctx = [int(c) + 1 for c in wl.prefix]
+    first = [c - 1 - 1024 for c in ctx]
+    ns = len(ctx)
+    shape = hswa.Shape(wl.hq, wl.hkv, D, wl.page_size)
+    layer = hswa.Layer.swa(wl.window)
+    kv = LayerKV(layer, shape, ctx, perm=synth.page_permutation(pages_for(layer, wl.page_size, ctx), wl.seed, 0))
+    n = 1024
+    kh = synth.normal_bf16((ns * n, wl.hkv, D), wl.seed, 0, synth.TAG_K)
+    vh = synth.normal_bf16((ns * n, wl.hkv, D), wl.seed, 0, synth.TAG_V)
+    hswa.kv_append(layer, shape, kv.cache, to_dev(kh), to_dev(vh), i32(synth.cu_seqlens([n] * ns)), i32(first))
+    kn = synth.normal_bf16((ns, wl.hkv, D), wl.seed, 0, synth.TAG_KDEC)
+    vn = synth.normal_bf16((ns, wl.hkv, D), wl.seed, 0, synth.TAG_VDEC)
+    qb = synth.normal_bf16((ns, wl.hq, D), wl.seed, 0, synth.TAG_QDEC)
+    out = torch.empty((ns, wl.hq, D), dtype=torch.bfloat16, device="cuda")
+    hswa.decode_append(layer, shape, kv.cache, to_dev(qb), to_dev(kn), to_dev(vn), i32(ctx), max(ctx), out)
+    torch.cuda.synchronize()
+    got = to_f64(out)
+    q = OA.bf16_bits_to_f64(qb)
+    for b in range(ns):
+        kf = OA.bf16_bits_to_f64(np.concatenate([kh[b * n:(b + 1) * n], kn[b:b + 1]]))
+        vf = OA.bf16_bits_to_f64(np.concatenate([vh[b * n:(b + 1) * n], vn[b:b + 1]]))
+        assert_close(got[b], OA.decode(q[b], kf, vf, wl.window), f"stack70 SWA seq {b}")
