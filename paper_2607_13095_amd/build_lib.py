@@ -63,5 +63,47 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+# Host-sanitizer build: the host code (the C ABI's validation in api.hip, the
+# allocator, the prefix tree) under gcc's address and undefined-behaviour
+# sanitizers, linked with the device objects of build(). Load it with the
+# sanitizer runtimes preloaded (sanitizer_env) and HSWA_LIB naming it.
+SAN_FLAGS = ["-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+             "-fno-sanitize-recover=undefined"]
+HIP_HOST_FLAGS = ["-D__HIP_PLATFORM_AMD__", "-I", "/opt/rocm/include"]
+
+
+def build_host_sanitized(out_dir: str) -> str:
+    """Build libhswa_san.so in out_dir; returns its path."""
+    dev_objs = [os.path.join(BUILD, s.replace(".hip", ".o")) for s in SOURCES if s != "api.hip"]
+    if not all(os.path.exists(o) for o in dev_objs):
+        build()
+    os.makedirs(out_dir, exist_ok=True)
+    # api.hip holds host code only; a one-line wrapper lets the host compiler take it as C++
+    wrap = os.path.join(out_dir, "api_host.cpp")
+    with open(wrap, "w") as f:
+        f.write(f'#include "{os.path.join(CSRC, "api.hip")}"\n')
+    units = [(wrap, HIP_HOST_FLAGS)] + [(os.path.join(CSRC, s), []) for s in HOST_SOURCES]
+    objs = []
+    for src, extra in units:
+        o = os.path.join(out_dir, os.path.basename(src) + ".san.o")
+        _run([CXX, "-std=c++17", "-fPIC", *SAN_FLAGS, *extra, "-I", os.path.join(ROOT, "include"), "-c", src, "-o", o])
+        objs.append(o)
+    lib = os.path.join(out_dir, "libhswa_san.so")
+    _run([CXX, "-shared", *SAN_FLAGS, "-o", lib, *objs, *dev_objs, "-L/opt/rocm/lib", "-lamdhip64",
+          "-Wl,-rpath,/opt/rocm/lib"])
+    return lib
+
+
+def sanitizer_env(lib: str) -> dict:
+    """Environment that runs Python with the sanitizer runtimes preloaded and
+    the binding loading `lib`."""
+    rt = [subprocess.run([CXX, f"-print-file-name={n}"], capture_output=True, text=True).stdout.strip()
+          for n in ("libasan.so", "libubsan.so")]
+    env = dict(os.environ)
+    env.update(LD_PRELOAD=" ".join(rt), HSWA_LIB=lib, ASAN_OPTIONS="detect_leaks=0",
+               UBSAN_OPTIONS="halt_on_error=1:print_stacktrace=1")
+    return env
+
+
 if __name__ == "__main__":
     print(build(verbose=True))

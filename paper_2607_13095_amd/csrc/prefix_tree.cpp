@@ -28,6 +28,24 @@ struct Node {
   std::vector<int64_t> full, swa;  // per token: slot or -1
   std::map<int32_t, std::unique_ptr<Node>> kids;
 
+  Node() = default;
+  Node(const Node &) = delete;
+  Node &operator=(const Node &) = delete;
+  // A path may hold any number of branch points: descendants are detached
+  // onto a work list and freed one by one, so that freeing a subtree (at
+  // teardown, eviction or a cut) never recurses once per level.
+  ~Node() {
+    std::vector<std::unique_ptr<Node>> pending;
+    for (auto &kv : kids) pending.push_back(std::move(kv.second));
+    kids.clear();
+    while (!pending.empty()) {
+      std::unique_ptr<Node> n = std::move(pending.back());
+      pending.pop_back();
+      for (auto &kv : n->kids) pending.push_back(std::move(kv.second));
+      n->kids.clear();
+    }
+  }
+
   // Splits this node after its first `at` tokens; the tail becomes the only child.
   void split(size_t at) {
     auto tail = std::make_unique<Node>();
@@ -43,16 +61,23 @@ struct Node {
   }
 };
 
-int64_t count_tokens(const Node &n, int64_t *swa_valid) {
-  int64_t t = (int64_t)n.tok.size();
-  for (int64_t s : n.swa) *swa_valid += s >= 0;
-  for (const auto &kv : n.kids) t += count_tokens(*kv.second, swa_valid);
-  return t;
-}
+// Tokens, SWA-valid tokens and nodes of the subtree at n (n included), by an
+// explicit work list: no recursion, whatever the depth.
+struct SubtreeCount {
+  int64_t tokens = 0, swa_valid = 0, nodes = 0;
+};
 
-int64_t count_nodes(const Node &n) {
-  int64_t c = 1;
-  for (const auto &kv : n.kids) c += count_nodes(*kv.second);
+SubtreeCount count_subtree(const Node &n) {
+  SubtreeCount c;
+  std::vector<const Node *> todo{&n};
+  while (!todo.empty()) {
+    const Node *x = todo.back();
+    todo.pop_back();
+    ++c.nodes;
+    c.tokens += (int64_t)x->tok.size();
+    for (int64_t s : x->swa) c.swa_valid += s >= 0;
+    for (const auto &kv : x->kids) todo.push_back(kv.second.get());
+  }
   return c;
 }
 
@@ -192,35 +217,38 @@ hswa_status hswa_prefix_tree_evict(hswa_prefix_tree *t, const int32_t *tokens, i
   // Find the node holding position `keep` on this path and cut there.
   Node *node = &t->root;
   int64_t pos = 0;
-  while (true) {
-    auto it = node->kids.find(tokens[pos]);
-    if (it == node->kids.end()) break;  // nothing cached at or beyond keep on this path
-    Node *c = it->second.get();
-    size_t k = 0;
-    while (k < c->tok.size() && pos + (int64_t)k < n && c->tok[k] == tokens[pos + k] && pos + (int64_t)k < keep) ++k;
-    if (pos + (int64_t)k == keep) {
-      int64_t sv = 0;
-      if (k == 0) {  // the whole child subtree goes
-        cnt = count_tokens(*c, &sv);
-        node->kids.erase(it);
-      } else if (k < c->tok.size()) {  // cut inside the node: drop its tail and all children
-        if (c->tok[k] == tokens[pos + k]) {
-          c->split(k);
-          cnt = count_tokens(*c->kids.begin()->second, &sv);
-          c->kids.clear();
+  try {
+    while (true) {
+      auto it = node->kids.find(tokens[pos]);
+      if (it == node->kids.end()) break;  // nothing cached at or beyond keep on this path
+      Node *c = it->second.get();
+      size_t k = 0;
+      while (k < c->tok.size() && pos + (int64_t)k < n && c->tok[k] == tokens[pos + k] && pos + (int64_t)k < keep) ++k;
+      if (pos + (int64_t)k == keep) {
+        if (k == 0) {  // the whole child subtree goes
+          cnt = count_subtree(*c).tokens;
+          node->kids.erase(it);
+        } else if (k < c->tok.size()) {  // cut inside the node: drop its tail and all children
+          if (c->tok[k] == tokens[pos + k]) {
+            c->split(k);
+            cnt = count_subtree(*c->kids.begin()->second).tokens;
+            c->kids.clear();
+          }
+        } else {  // keep ends exactly after this node: drop the child that continues the path
+          auto it2 = c->kids.find(tokens[keep]);
+          if (it2 != c->kids.end()) {
+            cnt = count_subtree(*it2->second).tokens;
+            c->kids.erase(it2);
+          }
         }
-      } else {  // keep ends exactly after this node: drop the child that continues the path
-        auto it2 = c->kids.find(tokens[keep]);
-        if (it2 != c->kids.end()) {
-          cnt = count_tokens(*it2->second, &sv);
-          c->kids.erase(it2);
-        }
+        break;
       }
-      break;
+      if (k < c->tok.size()) break;  // the path diverges before keep
+      pos += (int64_t)k;
+      node = c;
     }
-    if (k < c->tok.size()) break;  // the path diverges before keep
-    pos += (int64_t)k;
-    node = c;
+  } catch (...) {  // the count's work list could not grow (a split before it keeps the tree valid)
+    return HSWA_ERR_CAPACITY;
   }
   if (evicted) *evicted = cnt;
   return HSWA_OK;
@@ -229,11 +257,15 @@ hswa_status hswa_prefix_tree_evict(hswa_prefix_tree *t, const int32_t *tokens, i
 hswa_status hswa_prefix_tree_stats(const hswa_prefix_tree *t, int64_t *nodes, int64_t *tokens,
                                    int64_t *swa_valid_tokens) {
   if (!t) return HSWA_ERR_INVALID_ARG;
-  int64_t sv = 0;
-  const int64_t tk = count_tokens(t->root, &sv);
-  if (nodes) *nodes = count_nodes(t->root) - 1;
-  if (tokens) *tokens = tk;
-  if (swa_valid_tokens) *swa_valid_tokens = sv;
+  SubtreeCount c;
+  try {
+    c = count_subtree(t->root);
+  } catch (...) {
+    return HSWA_ERR_CAPACITY;
+  }
+  if (nodes) *nodes = c.nodes - 1;  // the root holds no tokens
+  if (tokens) *tokens = c.tokens;
+  if (swa_valid_tokens) *swa_valid_tokens = c.swa_valid;
   return HSWA_OK;
 }
 

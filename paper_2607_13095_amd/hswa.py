@@ -16,7 +16,8 @@ from typing import Optional, Sequence
 import numpy as np
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libhswa.so")
+# HSWA_LIB names another build of the same library (the host-sanitizer build)
+LIB_PATH = os.environ.get("HSWA_LIB") or os.path.join(_PKG, "libhswa.so")
 
 HSWA_LAYER_FULL = 0
 HSWA_LAYER_SWA = 1
