@@ -22,8 +22,11 @@
 // K pool stores each 32-key block in that row order, so every K load
 // instruction reads one contiguous 1 KiB (and every V load as well).
 // Softmax is online per chunk in fp32 (exp2 with scale*log2(e) folded in).
-// The K loads of chunk c+1 are in flight while chunk c's softmax and PV run,
-// its V loads while chunk c+1's QK^T runs. A segment cut by span boundaries
+// FULL split spans run one wave per SIMD with two whole chunks of loads in
+// flight while a third is computed (fewer, deeper streams read HBM faster
+// than more, shallower ones). Whole-range items: the K loads of chunk c+1 are
+// in flight while chunk c's softmax and PV run, its V loads while chunk c+1's
+// QK^T runs. A segment cut by span boundaries
 // gets fp32 (o, log2 sum-exp) partials that a second kernel merges; a segment
 // inside one span, and a whole-range item, is written as bf16 directly.
 #include <atomic>
@@ -122,14 +125,15 @@ constexpr int kWaves = 4;
 template <bool kSplit>
 constexpr int kCoop = kSplit ? 1 : kWaves;  // waves that share one item
 
-// kCGd: 16-column MFMA groups per wave. With one group (a single query, or
-// few query heads) a wave has at most 168 VGPRs, so that three waves share a
-// SIMD. With two groups (several queries: 32 (query, head) columns of a KV
-// head) one wave scores both against the same K/V loads, which halves the KV
-// bytes read; its accumulators double, so two waves share a SIMD.
+// kCGd: 16-column MFMA groups per wave. With two groups (several queries: 32
+// (query, head) columns of a KV head) one wave scores both against the same
+// K/V loads, which halves the KV bytes read. Whole-range items: with one group
+// a wave has at most 168 VGPRs, so that three waves share a SIMD (two with two
+// groups). Split spans with one page per chunk (PG >= 32): one wave per SIMD,
+// which leaves room for two chunks of operands in flight.
 template <bool kSplit, bool kOnePage, int kCGd>
-__global__ __launch_bounds__(kWave * kWaves) __attribute__((amdgpu_waves_per_eu(kCGd == 1 ? 3 : 2))) void
-decode_kernel(DecodeParams p) {
+__global__ __launch_bounds__(kWave * kWaves) __attribute__((amdgpu_waves_per_eu(kSplit && kOnePage ? 1 : (kCGd == 1 ? 3 : 2))))
+void decode_kernel(DecodeParams p) {
   const PoolView &pv = p.pool;
   const int lane = threadIdx.x & (kWave - 1);
   const int wid = threadIdx.x >> 6;  // wave of the workgroup
@@ -431,7 +435,40 @@ decode_kernel(DecodeParams p) {
         };
         // this wave's chunks: c0, c0 + kCoop, ...
         const int nw = nchunks > c0 ? (nchunks - c0 + kCoop<kSplit> - 1) / kCoop<kSplit> : 0;
-        if (nw > 0) {
+        if (kSplit && nw > 0) {
+          // Split spans (long streams of chunks): one wave per SIMD, two whole
+          // chunks in flight while a third is computed. Chunk k is computed
+          // while k + 1 is loaded and k + 2 is issued right after k's products;
+          // past the span's end the last chunk is loaded again (never used),
+          // so that every wait counts the same loads.
+          Chunk ca, cb;
+          auto issue_both = [&](int k, Chunk &ch) {
+            const int cc = c0 + k * kCoop<kSplit>;
+            const int page = page_of(cc);
+            issue_k(cc, page, ch);
+            issue_v(cc, page, ch);
+          };
+          issue_both(0, ca);
+          issue_both(min(1, nw - 1), cb);
+          u32x4 pf[kCGd];
+          int k = 0;
+          for (; k + 2 <= nw; k += 2) {
+            scores(ca, pf);
+            pv_update(ca, pf);
+            __builtin_amdgcn_sched_barrier(0);
+            issue_both(min(k + 2, nw - 1), ca);
+            __builtin_amdgcn_sched_barrier(0);
+            scores(cb, pf);
+            pv_update(cb, pf);
+            __builtin_amdgcn_sched_barrier(0);
+            issue_both(min(k + 3, nw - 1), cb);
+            __builtin_amdgcn_sched_barrier(0);
+          }
+          if (k < nw) {
+            scores(ca, pf);
+            pv_update(ca, pf);
+          }
+        } else if (nw > 0) {
           Chunk ch;
           {
             const int page = page_of(c0);

@@ -181,7 +181,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
     }
     return prefix_page(pv, b, j, ok);
   };
-  auto load_tile = [&](int kt, int tpage, Stage &st) {
+  auto load_tile = [&](int kt, int tpage, Stage &st) __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < kStage; ++i) {
       const int idx = tid + kThreads * i;
@@ -238,7 +238,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   // the same LDS byte as a pool piece. V piece i of lane l of wave w is key
   // 8 w + 4 i + l / 16, dims 8 (l % 16) .. +7; the store transposes those into
   // V^T (store_tile).
-  auto load_tile_chunk = [&](int kt, Stage &st) {
+  auto load_tile_chunk = [&](int kt, Stage &st) __attribute__((always_inline)) {
     const u32x4 z = {0u, 0u, 0u, 0u};
     const int r = lane & 15, ab = wave >> 2;
 #pragma unroll
@@ -262,7 +262,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   // id was fetched ahead; the K tile is two 8 KiB K blocks and the V tile two
   // [D][32] blocks of 8 KiB, all contiguous: plain 16-byte loads, consecutive
   // threads at consecutive addresses.
-  auto load_tile_page = [&](int kt, int page, Stage &st) {
+  auto load_tile_page = [&](int kt, int page, Stage &st) __attribute__((always_inline)) {
     const int64_t pg64 = max(page, 0);
     const int off = kt & (pg - 1);
     const uint16_t *kbase = pv.k_pool + k_offset(pv, pg64, hkv, g, off, 0);
@@ -299,7 +299,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
     w[2] = (uint32_t)d[0];
     w[3] = (uint32_t)d[1];
   };
-  auto store_tile = [&](int buf, const Stage &st) {
+  auto store_tile = [&](int buf, const Stage &st) __attribute__((always_inline)) {
     static_assert(kStage == 2, "two pieces per thread");
     const uint32_t bo = buf_off(buf);
     *lds128(bo + st_k0) = st.k[0];
@@ -374,7 +374,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
     }
     return __builtin_amdgcn_readlane(tab_page, lp - tab_lp0);
   };
-  auto fetch = [&](int kt, int page, Stage &st) {
+  auto fetch = [&](int kt, int page, Stage &st) __attribute__((always_inline)) {
     if (page >= 0 && interior(kt)) load_tile_page(kt, page, st);
     else if (kt >= P) load_tile_chunk(kt, st);
     else load_tile(kt, page, st);
@@ -493,30 +493,18 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
       for (int cg = 0; cg < kCG; ++cg) acc[cg][dt] = mfma16x16x32(vf[dt], pf[cg], acc[cg][dt]);
   };
 
-  // ---- ping-pong tile loop ----
+  // ---- tile loop ----
   // The waves form two groups, A (waves 0-3) and B (waves 4-7), one wave of
-  // each on every SIMD. A tile is processed in two phases separated by
-  // workgroup barriers: a matrix phase (QK^T of tile j and PV of tile j-1,
-  // both on MFMA, operands from LDS, plus this thread's share of the tile
-  // staging) and a softmax phase (VALU only). Group B runs one phase behind
-  // group A, so on every SIMD one wave's matrix products run while the other
-  // wave's exponentials do.
-  //
-  // Phase numbering: A runs the matrix phase of tile j in phase 2j and its
-  // softmax in 2j+1; B one phase later. Tile t is read in phases 2t..2t+3
-  // (K by A then B, V by A then B one tile later). The staging of the tiles
-  // (LDS stores, global loads, address arithmetic) runs in the softmax phases,
-  // which have the slack, so the matrix phases issue little else than MFMAs
-  // and their operand reads: each thread stores its share of tile t in its
-  // softmax phase of tile t-2 (phases 2t-3 and 2t-2), which a barrier
-  // separates from the first read (2t) and from the last read of the tile
-  // that used the buffer before (tile t-4: phase 2t-5). The global loads of a
-  // tile go out one tile before its store.
-  auto phase_barrier = [&]() {
-    __builtin_amdgcn_sched_barrier(0);
-    __syncthreads();
-    __builtin_amdgcn_sched_barrier(0);
-  };
+  // each on every SIMD. A tile is processed in two phases: a matrix phase
+  // (QK^T of tile j and PV of tile j-1, both on MFMA with operands from LDS)
+  // and a softmax phase (VALU: mask, exponentials, row sums, plus this
+  // thread's share of the tile staging: LDS stores, global loads, address
+  // arithmetic). Group B runs its phases offset from group A's (see the loop),
+  // so that on every SIMD one wave's matrix products overlap the other wave's
+  // softmax, and the two matrix phases overlap in part. Each thread stores its
+  // share of a tile two (group A) or one (group B) barrier intervals before
+  // the tile is first read; the global loads of a tile go out one tile before
+  // its store.
   auto pv_tile = [&](int buf, const u32x4 (&pf)[2][kCG]) {
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
@@ -536,16 +524,15 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   if (ntiles > 2) fetch(kt0 + 2 * kKT, tile_page(kt0 + 2 * kKT), st);
   __syncthreads();
   const bool lag = wave >= kThreads / kWave / 2;  // group B
-  if (lag) phase_barrier();
 
   f32x4 sc[2][2][kCG];
   u32x4 pf[2][kCG];
-  for (int jt = 0; jt < ntiles; ++jt) {
-    const int kt = kt0 + jt * kKT;
+  // matrix phase: PV of tile jt-1, QK^T of tile jt, at raised issue priority
+  // so that the other wave's softmax takes the issue slots the matrix
+  // products leave free
+  auto matrix_phase = [&](int jt) __attribute__((always_inline)) {
     const int buf = jt % kBufs;
-    // matrix phase: PV of tile jt-1, QK^T of tile jt, at raised issue priority
-    // so that the other wave's softmax takes the issue slots the matrix
-    // products leave free
+    __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_setprio(2);
     if (jt > 0) {
       pv_tile((jt + kBufs - 1) % kBufs, pf);
@@ -567,10 +554,13 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
       __builtin_amdgcn_sched_group_barrier(0x008, 2, 1);
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 2 * kAhead, 1);
-    phase_barrier();
+    __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_setprio(0);
-    // softmax phase, with this thread's share of the staging: tile jt+2 from
-    // registers to LDS, tile jt+3's global loads
+  };
+  // softmax phase of tile jt, with this thread's share of the staging: tile
+  // jt+2 from registers to LDS, tile jt+3's global loads
+  auto softmax_phase = [&](int jt) __attribute__((always_inline)) {
+    const int kt = kt0 + jt * kKT;
     if (jt + 2 < ntiles) store_tile((jt + 2) % kBufs, st);
     if (jt + 3 < ntiles) fetch(kt + 3 * kKT, tile_page(kt + 3 * kKT), st);
     if (needs_mask(kt)) {
@@ -578,10 +568,37 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
       mask_half(kt, 1, sc[1]);
     }
     softmax_tile(sc, pf);
-    phase_barrier();
+  };
+  // One barrier per tile. Between barriers t and t+1 group A runs the matrix
+  // phase of tile t, then its softmax phase; group B first the softmax phase
+  // of tile t-1, then the matrix phase of tile t. A wave of B thus starts its
+  // matrix products while its SIMD partner is still in its own, and the
+  // partner's softmax runs under the rest of them. Between those barriers the
+  // tiles read are t (K) and t-1 (V); the stores go to tile t+2 (group A) and
+  // t+1 (group B), whose buffers were last read (as tiles t-2 and t-3) before
+  // barrier t, and a stored tile is first read after a further barrier.
+  auto tile_barrier = [&]() {
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  if (!lag) {
+    for (int jt = 0; jt < ntiles; ++jt) {
+      matrix_phase(jt);
+      softmax_phase(jt);
+      tile_barrier();
+    }
+  } else {
+    matrix_phase(0);
+    tile_barrier();
+    for (int jt = 1; jt < ntiles; ++jt) {
+      softmax_phase(jt - 1);
+      matrix_phase(jt);
+      tile_barrier();
+    }
+    softmax_phase(ntiles - 1);
   }
   pv_tile((ntiles + kBufs - 1) % kBufs, pf);
-  if (!lag) phase_barrier();  // every wave passes the same number of barriers
 
   // ---- normalise and write ----
 #pragma unroll
