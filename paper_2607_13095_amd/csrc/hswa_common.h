@@ -146,6 +146,28 @@ __device__ __forceinline__ float sum_xor32(float x) {
 
 constexpr float kLog2e = 1.4426950408889634f;
 
+// Writes one output row from the MFMA accumulator layout: lane r + 16 q holds
+// dims 16 dt + 4 q .. +3 of row r as two bf16 pairs w[dt] (dt = 0..7). Lanes l
+// and l ^ 16 (same row) swap halves so that each holds 8 consecutive dims (dt
+// even in the lanes with q even, odd in the others); one 16-byte store then
+// writes a 64-byte run of each of the wave's 16 rows. The stores are
+// nontemporal: an output is written once and not read back. Every lane of the
+// wave must take part (the swaps are cross-lane); a lane with `write` false
+// (its partner has the same row, hence the same flag) stores nothing.
+__device__ __forceinline__ void store_out_row(uint16_t *orow, const u32x2 (&w)[8], int q, bool write) {
+  u32x4 v[4];
+#pragma unroll
+  for (int pp = 0; pp < 4; ++pp) {
+    const auto s0 = __builtin_amdgcn_permlane16_swap(w[2 * pp][0], w[2 * pp + 1][0], false, false);
+    const auto s1 = __builtin_amdgcn_permlane16_swap(w[2 * pp][1], w[2 * pp + 1][1], false, false);
+    v[pp] = u32x4{(uint32_t)s0[0], (uint32_t)s1[0], (uint32_t)s0[1], (uint32_t)s1[1]};
+  }
+  if (!write) return;
+#pragma unroll
+  for (int pp = 0; pp < 4; ++pp)
+    __builtin_nontemporal_store(v[pp], reinterpret_cast<u32x4 *>(orow + 32 * pp + 16 * (q & 1) + 8 * (q >> 1)));
+}
+
 // Launch a kernel taking one parameter struct and return the status of exactly
 // this launch (hipGetLastError would also report errors left behind by earlier,
 // unrelated runtime calls of the caller).

@@ -604,18 +604,17 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
 #pragma unroll
   for (int cg = 0; cg < kCG; ++cg) {
     const float l = sum_xor32(sum_xor16(lsum[cg]));
-    if (!cval[cg]) continue;
     const float inv = 1.f / l;
     const int row = wave * (16 * kCG) + cg * 16 + r;
     const int po = row / G, head = row - po * G;
-    uint16_t *orow = p.out + ((int64_t)(tok0 + q0 + po) * hq + (int64_t)g * G + head) * kHeadDim;
+    uint16_t *orow = p.out + ((int64_t)(tok0 + q0 + (cval[cg] ? po : 0)) * hq + (int64_t)g * G + head) * kHeadDim;
+    u32x2 w[8];
 #pragma unroll
     for (int dt = 0; dt < 8; ++dt) {
-      u32x2 w;
-      w[0] = pack_bf16x2(acc[cg][dt][0] * inv, acc[cg][dt][1] * inv);
-      w[1] = pack_bf16x2(acc[cg][dt][2] * inv, acc[cg][dt][3] * inv);
-      *reinterpret_cast<u32x2 *>(orow + 16 * dt + 4 * q) = w;
+      w[dt][0] = pack_bf16x2(acc[cg][dt][0] * inv, acc[cg][dt][1] * inv);
+      w[dt][1] = pack_bf16x2(acc[cg][dt][2] * inv, acc[cg][dt][3] * inv);
     }
+    store_out_row(orow, w, q, cval[cg]);
   }
 }
 

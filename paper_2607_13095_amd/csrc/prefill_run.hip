@@ -402,12 +402,10 @@ __global__ __launch_bounds__(kRThreads) __attribute__((amdgpu_waves_per_eu(4))) 
     // write this tile's rows
 #pragma unroll
     for (int cg = 0; cg < kRCG; ++cg) {
-      if (!kFull && !cval[cg]) continue;
       const int row = wave * (16 * kRCG) + cg * 16 + r;
       const int po = row / G, head = row - po * G;
-      uint16_t *orow = p.out + ((int64_t)(tok0 + q0 + po) * hq + (int64_t)g * G + head) * kHeadDim;
-#pragma unroll
-      for (int dt = 0; dt < 8; ++dt) *reinterpret_cast<u32x2 *>(orow + 16 * dt + 4 * q) = wo[cg][dt];
+      uint16_t *orow = p.out + ((int64_t)(tok0 + q0 + (kFull || cval[cg] ? po : 0)) * hq + (int64_t)g * G + head) * kHeadDim;
+      store_out_row(orow, wo[cg], q, kFull || cval[cg]);
     }
   };
   const int tfull = min(t1, C / npos);  // tiles before tfull hold npos valid positions
