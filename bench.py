@@ -55,11 +55,14 @@ FLUSH_BYTES = 1 << 30  # a write this large evicts the 256 MB memory-side cache
 # measured again.
 MEASURED_TRAFFIC = {
     "decode_full_stack70": {"sources": ["decode.hip", "hswa_common.h", "hswa_launch.h"],
-                            "sha256": "",
-                            "fetch_bytes": 0, "write_bytes": 0},
+                            "sha256": "13d68500ed422956e601499e5a6acd76855b074147037a96c9615d0e73ffd3a6",
+                            "fetch_bytes": 8610120847, "write_bytes": 5120045},
     "prefill_full": {"sources": ["prefill.hip", "hswa_common.h", "hswa_launch.h"],
-                     "sha256": "",
-                     "fetch_bytes": 0, "write_bytes": 0},
+                     "sha256": "3fd6169bdd42c875d5504d372684026131e986cc66ae5f12302da129e666bced",
+                     "fetch_bytes": 453122231, "write_bytes": 141538076},
+    "prefill_swa": {"sources": ["prefill_run.hip", "hswa_common.h", "hswa_launch.h"],
+                    "sha256": "0ec3136d4a24e36565e979acac7ee62b79bdfd47b5617eeba99ce8c6b5af775c",
+                    "fetch_bytes": 184792640, "write_bytes": 150198165},
 }
 
 
@@ -1092,6 +1095,7 @@ def main():
             "workload": pw.name, "full_ms": round(f_ms, 4), **{f"full_{k}": v for k, v in
                                                               rate(pb.bytes["full"], pb.flops["full"], f_ms).items()},
             "swa_ms": round(s_ms, 4), **{f"swa_{k}": v for k, v in rate(pb.bytes["swa"], pb.flops["swa"], s_ms).items()},
+            "swa_traffic": measured_traffic("prefill_swa"), "swa_algorithmic_bytes": pb.bytes["swa"],
             "roofline": {"bound": "mfma", "achieved": round(f_tf, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
                          "unit": "TFLOP/s", "frac": round(f_tf / MFMA_BF16_PEAK_TFLOPS, 4),
                          "traffic": measured_traffic("prefill_full"), "algorithmic_bytes": pb.bytes["full"],
