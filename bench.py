@@ -1,7 +1,7 @@
 """Benchmark of the hybrid-SWA paged attention hot path on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--no-prefill]
-                    [--roofline-only] [--copy-calibration]
+                    [--roofline-only] [--prefill-only] [--copy-calibration]
 
 Headline workload (the largest configuration that fits one GPU): a 70-layer
 hybrid decode step, 60 SWA layers (W = 128) and 10 FULL layers (FULL iff
@@ -97,6 +97,9 @@ def parse():
     ap.add_argument("--no-prefill", action="store_true")
     ap.add_argument("--roofline-only", action="store_true",
                     help="only the headline step and the prefill calls the roofline entries time (for counter runs)")
+    ap.add_argument("--prefill-only", action="store_true",
+                    help="only the chunked-prefill calls (FULL and SWA, timed back to back) and their power and "
+                         "clock telemetry; prints a JSON line with that entry alone (for counter runs)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="target oracle time of the headline CPU baseline")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 1 GiB device copy three times (reference for HBM byte counters)")
@@ -160,6 +163,60 @@ def time_calls(fn, flush, reps=20, warmup=3):
     ts = np.asarray(ts)
     return {"ms_median": round(float(np.median(ts)), 5), "ms_p10": round(float(np.percentile(ts, 10)), 5),
             "ms_p90": round(float(np.percentile(ts, 90)), 5), "reps": reps, "mall_flushed": True}
+
+
+def power_telemetry(fn, seconds=1.2):
+    """Socket power and reported gfx clock while `fn` runs back to back for
+    about `seconds` (amdsmi, polled every 5 ms from a host thread; the SMU's
+    metrics table lags by a few hundred ms, so only the second half of the
+    window counts). None where amdsmi is not usable."""
+    import threading
+
+    import torch
+
+    try:
+        import amdsmi
+
+        amdsmi.amdsmi_init()
+    except Exception as e:  # no SMU access on this host
+        log(f"[bench] power telemetry unavailable: {e!r}")
+        return None
+    try:
+        h = amdsmi.amdsmi_get_processor_handles()[0]
+        cap_w = amdsmi.amdsmi_get_power_cap_info(h)["power_cap"] / 1e6
+        samples, stop = [], threading.Event()
+
+        def poll():
+            while not stop.is_set():
+                m = amdsmi.amdsmi_get_gpu_metrics_info(h)
+                samples.append((time.perf_counter(), float(np.mean(m["current_gfxclks"])),
+                                float(m["current_socket_power"])))
+                time.sleep(0.005)
+
+        th = threading.Thread(target=poll)
+        th.start()
+        t0 = time.perf_counter()
+        calls = 0
+        while time.perf_counter() - t0 < seconds:
+            for _ in range(20):
+                fn()
+            calls += 20
+            torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        stop.set()
+        th.join()
+        s = np.asarray([x for x in samples if (t0 + t1) / 2 <= x[0] <= t1])
+        if len(s) == 0:
+            return None
+        return {"socket_power_w": round(float(s[:, 2].mean()), 1), "power_cap_w": round(cap_w, 1),
+                "gfxclk_mhz_reported": round(float(s[:, 1].mean()), 1), "samples": int(len(s)), "calls": calls,
+                "note": "amdsmi metrics over the second half of ~1 s of back-to-back calls (the SMU's reported "
+                        "clock; rocprofv3's GRBM_GUI_ACTIVE per XCD over the kernel time gives the effective one)"}
+    except Exception as e:
+        log(f"[bench] power telemetry failed: {e!r}")
+        return None
+    finally:
+        amdsmi.amdsmi_shut_down()
 
 
 def time_back_to_back(fn, reps, warmup=2):
@@ -1026,6 +1083,53 @@ def headline(args, flush):
     return out
 
 
+def prefill_section(args, flush):
+    """The chunked-prefill entry: FULL and SWA calls timed back to back (the
+    FULL one is the MFMA roofline entry), their power and clock telemetry, and
+    (outside --roofline-only / --prefill-only) the flushed per-call timings,
+    the layerwise prefetch and the prefill CPU baseline."""
+    import torch
+
+    import synth
+
+    pw = synth.chunked_prefill_4x8k()
+    log(f"[bench] setting up {pw.name}")
+    pb = PrefillBench(pw)
+    Lf, Ls = pb.kind("full"), pb.kind("swa")
+    f_ms = time_back_to_back(lambda: pb.call(Lf), 20, warmup=10)
+    s_ms = time_back_to_back(lambda: pb.call(Ls), 20, warmup=10)
+    f_tf = pb.flops["full"] / (f_ms * 1e-3) / 1e12
+    prefill = {
+        "workload": pw.name, "full_ms": round(f_ms, 4), **{f"full_{k}": v for k, v in
+                                                          rate(pb.bytes["full"], pb.flops["full"], f_ms).items()},
+        "swa_ms": round(s_ms, 4), **{f"swa_{k}": v for k, v in rate(pb.bytes["swa"], pb.flops["swa"], s_ms).items()},
+        "swa_traffic": measured_traffic("prefill_swa"), "swa_algorithmic_bytes": pb.bytes["swa"],
+        "roofline": {"bound": "mfma", "achieved": round(f_tf, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(f_tf / MFMA_BF16_PEAK_TFLOPS, 4),
+                     "traffic": measured_traffic("prefill_full"), "algorithmic_bytes": pb.bytes["full"],
+                     "algorithmic_flops": pb.flops["full"], "kernel": "prefill_kernel (FULL layer call)"},
+    }
+    log(f"[bench] prefill FULL {f_ms:.3f} ms = {f_tf:.1f} TFLOP/s; SWA {s_ms:.4f} ms")
+    if not args.roofline_only:
+        # the power and clock this MFMA-bound call runs at differ from box to
+        # box, and so does its rate
+        prefill["full_power"] = power_telemetry(lambda: pb.call(Lf))
+        log(f"[bench] FULL prefill power: {prefill['full_power']}")
+    if not args.roofline_only and not args.prefill_only:
+        prefill["full_call"] = time_calls(lambda: pb.call(Lf), flush)
+        prefill["swa_call"] = time_calls(lambda: pb.call(Ls), flush)
+        log("[bench] layerwise prefetch (70-layer prefill stack, prefix from pinned host memory)")
+        prefill["prefetch"] = prefetch_report(pb)
+        log(f"[bench] prefetch: {prefill['prefetch']}")
+        if not args.no_cpu_baseline:
+            log("[bench] prefill CPU baseline")
+            prefill["cpu_baseline"] = pb.cpu_baseline()
+            log(f"[bench] prefill CPU baseline: {prefill['cpu_baseline']}")
+    del pb
+    torch.cuda.empty_cache()
+    return prefill
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -1042,6 +1146,14 @@ def main():
     if args.copy_calibration:
         copy_calibration()
     flush = MallFlush()
+
+    if args.prefill_only:
+        prefill = prefill_section(args, flush)
+        print(json.dumps({"metric": "prefill attn TFLOP/s (% MFMA), W=128", "value": prefill["roofline"]["achieved"],
+                          "unit": "TFLOP/s", "n_gpus": 1, "higher_is_better": True, "dtype": "bf16",
+                          "data": "synthetic", "config": {"workload": prefill["workload"]}, "prefill": prefill}),
+              flush=True)
+        return
 
     h = headline(args, flush)
     st = h["st"]
@@ -1082,38 +1194,7 @@ def main():
         swa512 = swa512_report(flush, cpu=not args.no_cpu_baseline)
         log(f"[bench] swa_prefill_512: {swa512}")
 
-    prefill = None
-    if not args.no_prefill:
-        pw = synth.chunked_prefill_4x8k()
-        log(f"[bench] setting up {pw.name}")
-        pb = PrefillBench(pw)
-        Lf, Ls = pb.kind("full"), pb.kind("swa")
-        f_ms = time_back_to_back(lambda: pb.call(Lf), 20, warmup=10)
-        s_ms = time_back_to_back(lambda: pb.call(Ls), 20, warmup=10)
-        f_tf = pb.flops["full"] / (f_ms * 1e-3) / 1e12
-        prefill = {
-            "workload": pw.name, "full_ms": round(f_ms, 4), **{f"full_{k}": v for k, v in
-                                                              rate(pb.bytes["full"], pb.flops["full"], f_ms).items()},
-            "swa_ms": round(s_ms, 4), **{f"swa_{k}": v for k, v in rate(pb.bytes["swa"], pb.flops["swa"], s_ms).items()},
-            "swa_traffic": measured_traffic("prefill_swa"), "swa_algorithmic_bytes": pb.bytes["swa"],
-            "roofline": {"bound": "mfma", "achieved": round(f_tf, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
-                         "unit": "TFLOP/s", "frac": round(f_tf / MFMA_BF16_PEAK_TFLOPS, 4),
-                         "traffic": measured_traffic("prefill_full"), "algorithmic_bytes": pb.bytes["full"],
-                         "algorithmic_flops": pb.flops["full"], "kernel": "prefill_kernel (FULL layer call)"},
-        }
-        log(f"[bench] prefill FULL {f_ms:.3f} ms = {f_tf:.1f} TFLOP/s; SWA {s_ms:.4f} ms")
-        if not args.roofline_only:
-            prefill["full_call"] = time_calls(lambda: pb.call(Lf), flush)
-            prefill["swa_call"] = time_calls(lambda: pb.call(Ls), flush)
-            log("[bench] layerwise prefetch (70-layer prefill stack, prefix from pinned host memory)")
-            prefill["prefetch"] = prefetch_report(pb)
-            log(f"[bench] prefetch: {prefill['prefetch']}")
-            if not args.no_cpu_baseline:
-                log("[bench] prefill CPU baseline")
-                prefill["cpu_baseline"] = pb.cpu_baseline()
-                log(f"[bench] prefill CPU baseline: {prefill['cpu_baseline']}")
-        del pb
-        torch.cuda.empty_cache()
+    prefill = None if args.no_prefill else prefill_section(args, flush)
 
     mtp = prefix_rep = alloc_rep = mixed = None
     if not args.roofline_only:
