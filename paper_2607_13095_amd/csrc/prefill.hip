@@ -262,16 +262,26 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   // id was fetched ahead; the K tile is two 8 KiB K blocks and the V tile two
   // [D][32] blocks of 8 KiB, all contiguous: plain 16-byte loads, consecutive
   // threads at consecutive addresses.
+  // The tile's two base addresses are wave-uniform (scalar registers) and each
+  // load adds a fixed 32-bit per-lane byte offset, so the loads take the
+  // scalar-base form with no per-tile vector address arithmetic.
+  // (The empty asm keeps the offsets opaque: the compiler would otherwise fold
+  // the constant 8 KiB step between a thread's two pieces into 64-bit vector
+  // address arithmetic.)
+  uint32_t pg_koff[kStage] = {(uint32_t)tid * 16u, (uint32_t)(tid + kThreads) * 16u};
+  uint32_t pg_voff[kStage] = {(uint32_t)(v_piece_dim(tid) * 32 + ((tid >> 4) & 3) * 8) * 2u,
+                              (uint32_t)(32 * kHeadDim + v_piece_dim(tid) * 32 + ((tid >> 4) & 3) * 8) * 2u};
+#pragma unroll
+  for (int i = 0; i < kStage; ++i) asm volatile("" : "+v"(pg_koff[i]), "+v"(pg_voff[i]));
   auto load_tile_page = [&](int kt, int page, Stage &st) __attribute__((always_inline)) {
     const int64_t pg64 = max(page, 0);
     const int off = kt & (pg - 1);
-    const uint16_t *kbase = pv.k_pool + k_offset(pv, pg64, hkv, g, off, 0);
-    const uint16_t *vbase = pv.v_pool + v_offset(pv, pg64, hkv, g, off, 0);
+    const char *kbase = reinterpret_cast<const char *>(pv.k_pool + k_offset(pv, pg64, hkv, g, off, 0));
+    const char *vbase = reinterpret_cast<const char *>(pv.v_pool + v_offset(pv, pg64, hkv, g, off, 0));
 #pragma unroll
     for (int i = 0; i < kStage; ++i) {
-      const int idx = tid + kThreads * i;
-      st.k[i] = ldg128(kbase + idx * 8);
-      st.v[i] = ldg128(vbase + i * (32 * kHeadDim) + v_piece_dim(tid) * 32 + ((tid >> 4) & 3) * 8);
+      st.k[i] = ldg128_global(kbase + pg_koff[i]);
+      st.v[i] = ldg128_global(vbase + pg_voff[i]);
     }
     st.vrow = false;
   };
@@ -299,31 +309,32 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
     w[2] = (uint32_t)d[0];
     w[3] = (uint32_t)d[1];
   };
-  auto store_tile = [&](int buf, const Stage &st) __attribute__((always_inline)) {
+  auto store_tile = [&](int buf, Stage &st) __attribute__((always_inline)) {
     static_assert(kStage == 2, "two pieces per thread");
     const uint32_t bo = buf_off(buf);
     *lds128(bo + st_k0) = st.k[0];
     *lds128(bo + st_k0 + kKTileBytes / 2) = st.k[1];
-    if (!st.vrow) {
-      *lds128(bo + st_v0) = st.v[0];
-      *lds128(bo + st_v0 + kKTileBytes / 2) = st.v[1];
-    } else {
+    if (st.vrow) {
       // The lanes l % 16 + 16 m (m = 0..3) of a wave hold an 8 x 8 block: keys
       // 8 w + 4 i + m (piece i) x dims 8 (l % 16) .. +7. After the transposes
       // lane m holds dims 2 m, 2 m + 1 of keys 8 w .. +7 (w[k]); byte permutes
-      // split them into one V^T piece per dim.
+      // split them into one V^T piece per dim, which replace the pieces in
+      // place (so both kinds of tile store the same registers and the stores
+      // need no copies).
       uint32_t w[8];
       transpose4(st.v[0], *reinterpret_cast<uint32_t(*)[4]>(&w[0]));
       transpose4(st.v[1], *reinterpret_cast<uint32_t(*)[4]>(&w[4]));
-      u32x4 lo, hi;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        lo[j] = __builtin_amdgcn_perm(w[2 * j + 1], w[2 * j], 0x05040100u);
-        hi[j] = __builtin_amdgcn_perm(w[2 * j + 1], w[2 * j], 0x07060302u);
+        st.v[0][j] = __builtin_amdgcn_perm(w[2 * j + 1], w[2 * j], 0x05040100u);
+        st.v[1][j] = __builtin_amdgcn_perm(w[2 * j + 1], w[2 * j], 0x07060302u);
       }
-      *lds128(bo + st_vrow0) = lo;
-      *lds128(bo + st_vrow0 + 16) = hi;
     }
+    // V^T pieces: a pool tile's two pieces sit 8 KiB apart at st_v0, a chunk
+    // tile's 16 bytes apart at st_vrow0
+    const uint32_t va = bo + (st.vrow ? st_vrow0 : st_v0);
+    *lds128(va) = st.v[0];
+    *lds128(va + (uint32_t)__builtin_amdgcn_readfirstlane(st.vrow ? 16 : kKTileBytes / 2)) = st.v[1];
   };
 
   float m[kCG], lsum[kCG];  // m: running maximum in exp2 units
