@@ -915,7 +915,8 @@ def mixed_report(reps=10, warmup=3):
     then the decodes' append and decode. Reports each call's rate and the step
     time against the sum of the calls' rooflines (one stream) and against the
     larger of the prefill and decode rooflines (the bound if the two ran
-    overlapped on two streams)."""
+    overlapped on two streams), and the step run that way: the prefill chain
+    on the current stream, the decode chain on a second one."""
     import torch
 
     import synth
@@ -984,10 +985,28 @@ def mixed_report(reps=10, warmup=3):
             prefill(L)
             decode(L)
 
+    # The same step with the prefill chain (every layer's prefill + append) on
+    # the current stream and the decode chain on a second stream of the same
+    # (default) priority: the two touch disjoint sequences, so a serving loop
+    # may overlap them; the decode's memory traffic then runs beside the
+    # prefill's matrix work wherever the scheduler gives it CUs.
+    side = torch.cuda.Stream()
+
+    def step_two_streams():
+        main = torch.cuda.current_stream()
+        side.wait_stream(main)
+        with torch.cuda.stream(side):
+            for L in layers:
+                decode(L)
+        for L in layers:
+            prefill(L)
+        main.wait_stream(side)
+
     by = {L["kind"]: L for L in layers}
     t = {f"{what}_{k}": time_back_to_back(lambda f=f, L=L: f(L), reps, warmup) for k, L in by.items()
          for what, f in (("prefill", prefill), ("decode", decode))}
     step_ms = time_back_to_back(step, reps, warmup)
+    step2_ms = time_back_to_back(step_two_streams, reps, warmup)
     row, hd = hkv * d * 2 * 2, 4 * d * hq
     flops, pbytes, dbytes = {}, {}, {}
     for k in by:
@@ -1008,6 +1027,8 @@ def mixed_report(reps=10, warmup=3):
         "roofline_sum_ms": round(pre_roof + dec_roof, 4), "frac_of_roofline": round((pre_roof + dec_roof) / step_ms, 4),
         "roofline_two_stream_ms": round(max(pre_roof, dec_roof), 4),
         "frac_of_two_stream_roofline": round(max(pre_roof, dec_roof) / step_ms, 4),
+        "step_two_streams_ms": round(step2_ms, 4),
+        "frac_of_two_stream_roofline_overlapped": round(max(pre_roof, dec_roof) / step2_ms, 4),
         "prefill_full_ms": round(t["prefill_full"], 4),
         "prefill_full_tflops": round(flops["full"] / (t["prefill_full"] * 1e-3) / 1e12, 1),
         "prefill_swa_ms": round(t["prefill_swa"], 4),
