@@ -1117,8 +1117,10 @@ def prefill_section(args, flush):
     log(f"[bench] setting up {pw.name}")
     pb = PrefillBench(pw)
     Lf, Ls = pb.kind("full"), pb.kind("swa")
-    f_ms = time_back_to_back(lambda: pb.call(Lf), 20, warmup=10)
-    s_ms = time_back_to_back(lambda: pb.call(Ls), 20, warmup=10)
+    # The clock settles over the first ~20 FULL calls (~50 ms of matrix-core
+    # load): time the calls after 40 untimed ones (the SWA call after 200).
+    f_ms = time_back_to_back(lambda: pb.call(Lf), 20, warmup=40)
+    s_ms = time_back_to_back(lambda: pb.call(Ls), 20, warmup=200)
     f_tf = pb.flops["full"] / (f_ms * 1e-3) / 1e12
     prefill = {
         "workload": pw.name, "full_ms": round(f_ms, 4), **{f"full_{k}": v for k, v in
