@@ -42,7 +42,8 @@ constexpr int kRows = 256;  // query rows per workgroup
 constexpr int kKT = 64;     // keys per tile
 constexpr int kCG = 2;      // 16-column MFMA groups per wave
 constexpr int kXcds = 8;
-constexpr int kBufs = 4;  // LDS tile buffers: two being read, one stored, one loading
+constexpr int kBufs = 4;  // LDS tile buffers (a power of two): two being read, one stored, one loading
+static_assert((kBufs & (kBufs - 1)) == 0, "buffer indices are taken modulo kBufs with a mask");
 // a lane's share (16 probabilities) of a row sum above which the running
 // maximum is raised
 constexpr float kLaneSumLimit = 4096.f;
@@ -273,11 +274,17 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
                               (uint32_t)(32 * kHeadDim + v_piece_dim(tid) * 32 + ((tid >> 4) & 3) * 8) * 2u};
 #pragma unroll
   for (int i = 0; i < kStage; ++i) asm volatile("" : "+v"(pg_koff[i]), "+v"(pg_voff[i]));
+  // For a tile on one page (PG >= 64, in-page offset a multiple of 64) both
+  // pools put the page-head at the same byte offset, page * (Hkv PG D 2) +
+  // g * (PG D 2), and its 32-key blocks 8 KiB apart: one scalar offset serves
+  // the K and the V loads.
+  const uint32_t page_bytes = (uint32_t)hkv << (shift + kHeadDimShift + 1);
+  const uint64_t head_bytes = (uint64_t)g << (shift + kHeadDimShift + 1);
   auto load_tile_page = [&](int kt, int page, Stage &st) __attribute__((always_inline)) {
-    const int64_t pg64 = max(page, 0);
-    const int off = kt & (pg - 1);
-    const char *kbase = reinterpret_cast<const char *>(pv.k_pool + k_offset(pv, pg64, hkv, g, off, 0));
-    const char *vbase = reinterpret_cast<const char *>(pv.v_pool + v_offset(pv, pg64, hkv, g, off, 0));
+    const uint64_t o = (uint64_t)(uint32_t)max(page, 0) * page_bytes + head_bytes +
+                       (uint64_t)(((uint32_t)kt & (uint32_t)(pg - 1)) >> 5) * 8192u;
+    const char *kbase = reinterpret_cast<const char *>(pv.k_pool) + o;
+    const char *vbase = reinterpret_cast<const char *>(pv.v_pool) + o;
 #pragma unroll
     for (int i = 0; i < kStage; ++i) {
       st.k[i] = ldg128_global(kbase + pg_koff[i]);
@@ -542,11 +549,11 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   // so that the other wave's softmax takes the issue slots the matrix
   // products leave free
   auto matrix_phase = [&](int jt) __attribute__((always_inline)) {
-    const int buf = jt % kBufs;
+    const int buf = jt & (kBufs - 1);
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_setprio(2);
     if (jt > 0) {
-      pv_tile((jt + kBufs - 1) % kBufs, pf);
+      pv_tile((jt + kBufs - 1) & (kBufs - 1), pf);
       // operand reads run kAhead reads ahead of the products that use them
       __builtin_amdgcn_sched_group_barrier(0x100, kAhead, 0);
 #pragma unroll
@@ -572,7 +579,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   // jt+2 from registers to LDS, tile jt+3's global loads
   auto softmax_phase = [&](int jt) __attribute__((always_inline)) {
     const int kt = kt0 + jt * kKT;
-    if (jt + 2 < ntiles) store_tile((jt + 2) % kBufs, st);
+    if (jt + 2 < ntiles) store_tile((jt + 2) & (kBufs - 1), st);
     if (jt + 3 < ntiles) fetch(kt + 3 * kKT, tile_page(kt + 3 * kKT), st);
     if (needs_mask(kt)) {
       mask_half(kt, 0, sc[0]);
@@ -609,7 +616,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
     }
     softmax_phase(ntiles - 1);
   }
-  pv_tile((ntiles + kBufs - 1) % kBufs, pf);
+  pv_tile((ntiles + kBufs - 1) & (kBufs - 1), pf);
 
   // ---- normalise and write ----
 #pragma unroll
