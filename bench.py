@@ -244,6 +244,10 @@ def rate(nbytes=None, flops=None, ms=None):
     if flops is not None:
         tf = flops / (ms * 1e-3) / 1e12
         out.update(tflops=round(tf, 2), frac_mfma=round(tf / MFMA_BF16_PEAK_TFLOPS, 4))
+    if nbytes is not None and flops is not None:
+        # the binding roofline: the larger of the two floors, over the time
+        floor_ms = max(flops / (MFMA_BF16_PEAK_TFLOPS * 1e12), nbytes / (HBM_PEAK_GBS * 1e9)) * 1e3
+        out.update(frac_binding=round(floor_ms / ms, 4))
     return out
 
 
