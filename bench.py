@@ -58,11 +58,11 @@ MEASURED_TRAFFIC = {
                             "sha256": "13d68500ed422956e601499e5a6acd76855b074147037a96c9615d0e73ffd3a6",
                             "fetch_bytes": 8610120847, "write_bytes": 5120045},
     "prefill_full": {"sources": ["prefill.hip", "hswa_common.h", "hswa_launch.h"],
-                     "sha256": "cf5155d962a733f11837de8101ff48f4d77ab884dd94f941742925edcfa6b74c",
-                     "fetch_bytes": 452812800, "write_bytes": 141572813},
+                     "sha256": "429ca9af748eed0f086aa376fae1438b67f47859ecc5d0ce2e0fb480aa0a21b7",
+                     "fetch_bytes": 452782694, "write_bytes": 141586330},
     "prefill_swa": {"sources": ["prefill_run.hip", "hswa_common.h", "hswa_launch.h"],
                     "sha256": "0ec3136d4a24e36565e979acac7ee62b79bdfd47b5617eeba99ce8c6b5af775c",
-                    "fetch_bytes": 184789402, "write_bytes": 149623910},
+                    "fetch_bytes": 184793088, "write_bytes": 149660365},
 }
 
 
