@@ -138,3 +138,47 @@ def test_random_decode_multi(gpu_lib, seed):
     for b, c in enumerate(ctxs):
         ref = OA.prefill(qf[b], OA.bf16_bits_to_f64(hist.k[b]), OA.bf16_bits_to_f64(hist.v[b]), c, w, scale)
         assert_close(gpu[b], ref, f"multi seed {seed} seq {b}")
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_random_append(gpu_lib, seed):
+    """Random batches of append calls (empty and single-token appends
+    included): the slot mapping and every byte of both pools, NaN-filled at
+    the start, match the layout oracle after every call."""
+    from oracle import layout as OL
+    from tests.hswa_testlib import to_bits
+
+    rng = np.random.default_rng(9300 + seed)
+    pg = int(rng.choice([16, 32, 64, 128, 256]))
+    hkv = int(rng.choice([1, 2, 4, 8]))
+    ns = int(rng.integers(1, 7))
+    ncalls = int(rng.integers(1, 5))
+    calls, pos = [], [0] * ns
+    for _ in range(ncalls):
+        call = []
+        for b in range(ns):
+            n = int(rng.choice([0, 1, int(rng.integers(1, 700))]))
+            call.append((pos[b], pos[b] + n))
+            pos[b] += n
+        calls.append(call)
+    final = [max(1, p) for p in pos]
+    kind, window = draw_layer(rng, max(final))
+    print(f"[sweep-append] seed={seed} kind={kind} W={window} pg={pg} hkv={hkv} ns={ns} calls={ncalls} "
+          f"final={final}", flush=True)
+    shape = hswa.Shape(hkv, hkv, D, pg)
+    layer, kv = make_layer(kind, window, shape, final, (9300, seed))
+    hist = SeqHistory(final, hkv, D, 9300, seed)
+    exp_k, exp_v = to_bits(kv.k_pool), to_bits(kv.v_pool)
+    okind = OL.SWA if kind == "swa" else OL.FULL
+    for ci, call in enumerate(calls):
+        starts = [s for s, _ in call]
+        slots = append_history(layer, shape, kv, hist, starts, [e for _, e in call])
+        exp_slots = OL.slot_mapping(okind, window or None, pg, kv.table_host, starts, [e - s for s, e in call])
+        assert np.array_equal(slots, exp_slots), f"slot mapping differs, call {ci}"
+        if len(exp_slots):
+            kn = np.concatenate([hist.k[b][s:e] for b, (s, e) in enumerate(call)])
+            vn = np.concatenate([hist.v[b][s:e] for b, (s, e) in enumerate(call)])
+            exp_k, exp_v = OL.apply_append(exp_k, exp_v, exp_slots, kn, vn)
+        torch.cuda.synchronize()
+        assert np.array_equal(to_bits(kv.k_pool), exp_k), f"K pool differs after call {ci}"
+        assert np.array_equal(to_bits(kv.v_pool), exp_v), f"V pool differs after call {ci}"
