@@ -686,6 +686,67 @@ class PrefillBench:
 
 # ----------------------------------------------------------------------------
 # swa_prefill_512 (one SWA layer, no cache, 8 / 1 heads, page size 16)
+def prefix_sweep_report(prefixes=(0, 16384, 65536, 262144, 1048576), chunk=16384):
+    """FULL-layer prefill of one 16K-token chunk (64 / 8 heads, PG 64) over
+    cached prefixes from 0 to 1M: time, TFLOP/s and tokens/s against the empty
+    prefix. Context for the paper's prefill-throughput-vs-prefix figure, which
+    is end to end (the rest of its model costs the same per token at any
+    prefix); this is the FULL layer's attention alone, whose work grows with
+    the prefix, so its tokens/s falls much further. The prefix's keys are
+    synthetic values in the pages, drawn once for the longest prefix."""
+    import torch
+
+    import synth
+    from paper_2607_13095_amd import hswa
+    from paper_2607_13095_amd.kvcache import LayerKV, pages_for
+
+    hq, hkv, d, pg = 64, 8, 128, 64
+    shape = hswa.Shape(hq, hkv, d, pg)
+    layer = hswa.Layer.full()
+    final = [max(prefixes) + chunk]
+    kv = LayerKV(layer, shape, final, perm=synth.page_permutation(pages_for(layer, pg, final), 17, 0))
+    i32 = lambda x: torch.as_tensor(np.asarray(x, dtype=np.int32), device="cuda")  # noqa: E731
+    P = max(prefixes)
+    step_keys = 1 << 18
+    for s0 in range(0, P, step_keys):  # the cached keys, a quarter million at a time
+        n = min(step_keys, P - s0)
+        kh = synth.torch_normal_bf16((n, hkv, d), "cuda", 17, 0, s0, synth.TAG_K)
+        vh = synth.torch_normal_bf16((n, hkv, d), "cuda", 17, 0, s0, synth.TAG_V)
+        hswa.kv_append(layer, shape, kv.cache, kh, vh, i32([0, n]), i32([s0]))
+        del kh, vh
+    q = synth.torch_normal_bf16((chunk, hq, d), "cuda", 17, 1, 0, synth.TAG_Q)
+    kn = synth.torch_normal_bf16((chunk, hkv, d), "cuda", 17, 1, 0, synth.TAG_K)
+    vn = synth.torch_normal_bf16((chunk, hkv, d), "cuda", 17, 1, 0, synth.TAG_V)
+    out = torch.empty((chunk, hq, d), dtype=torch.bfloat16, device="cuda")
+    cu = i32([0, chunk])
+    rows = []
+    for p0 in prefixes:
+        pre = i32([p0])
+
+        def call():
+            hswa.prefill(layer, shape, kv.cache, q, kn, vn, cu, pre, chunk, out)
+
+        # ~40 calls' worth of an empty-prefix call to warm up (the clock ramp),
+        # at least 2 calls; fewer timed calls for the long prefixes (0.5 s at 1M)
+        reps = 20 if p0 <= 65536 else 3
+        warm = max(2, min(40, (40 * 16) // (p0 // 1024 + 16)))
+        ms = time_back_to_back(call, reps, warmup=warm)
+        pairs = chunk * p0 + chunk * (chunk + 1) // 2
+        flops = 4 * d * hq * pairs
+        nbytes = (p0 + chunk) * hkv * d * 4 + 2 * chunk * hq * d * 2
+        rows.append({"prefix": p0, "ms": round(ms, 4), "tokens_per_s": round(chunk / (ms * 1e-3), 1),
+                     **rate(nbytes, flops, ms)})
+    base = rows[0]["tokens_per_s"]
+    for r in rows:
+        r["tokens_per_s_vs_empty_prefix"] = round(r["tokens_per_s"] / base, 5)
+    del kv, q, kn, vn, out
+    torch.cuda.empty_cache()
+    return {"workload": "prefill_16k_chunk_vs_prefix", "layer": "FULL, 64/8 heads, PG 64", "chunk": chunk,
+            "rows": rows,
+            "paper_context": "the paper's end-to-end prefill throughput at a 1M prefix is about 0.12x its "
+                             "throughput near an empty prefix (other hardware, whole model)"}
+
+
 # ----------------------------------------------------------------------------
 
 def swa512_report(flush, cpu=True):
@@ -1222,6 +1283,11 @@ def main():
         log(f"[bench] swa_prefill_512: {swa512}")
 
     prefill = None if args.no_prefill else prefill_section(args, flush)
+    prefix_sweep = None
+    if not args.no_prefill and not args.roofline_only:
+        log("[bench] FULL prefill of a 16K chunk over prefixes 0 .. 1M")
+        prefix_sweep = prefix_sweep_report()
+        log(f"[bench] prefix sweep: {[(r['prefix'], r['ms'], r.get('frac_mfma')) for r in prefix_sweep['rows']]}")
 
     mtp = prefix_rep = alloc_rep = mixed = None
     if not args.roofline_only:
@@ -1270,6 +1336,7 @@ def main():
         "decode_b64": decode_b64,
         "swa_prefill_512": swa512,
         "prefill": prefill,
+        "prefill_vs_prefix": prefix_sweep,
         "multi_query_decode": mtp,
         "allocator": alloc_rep,
         "prefix_tree": prefix_rep,
