@@ -58,8 +58,8 @@ MEASURED_TRAFFIC = {
                             "sha256": "13d68500ed422956e601499e5a6acd76855b074147037a96c9615d0e73ffd3a6",
                             "fetch_bytes": 8610120847, "write_bytes": 5120045},
     "prefill_full": {"sources": ["prefill.hip", "hswa_common.h", "hswa_launch.h"],
-                     "sha256": "429ca9af748eed0f086aa376fae1438b67f47859ecc5d0ce2e0fb480aa0a21b7",
-                     "fetch_bytes": 452782694, "write_bytes": 141586330},
+                     "sha256": "b5d6ebe3c313260bcd14426b0f9593b3a2ba6b4e399903c7cdc871b5705d7b4f",
+                     "fetch_bytes": 452820666, "write_bytes": 141551869},
     "prefill_swa": {"sources": ["prefill_run.hip", "hswa_common.h", "hswa_launch.h"],
                     "sha256": "0ec3136d4a24e36565e979acac7ee62b79bdfd47b5617eeba99ce8c6b5af775c",
                     "fetch_bytes": 184793088, "write_bytes": 149660365},

@@ -59,6 +59,9 @@ constexpr int kAhead = 6;  // LDS operand reads in flight ahead of the matrix pr
 //   V^T tile: block (h, dt) at 16 KiB + (8 h + dt) KiB holds, for lane r + 16 q,
 //     keys 32 h + 8 q .. +7 of dim 16 dt + r.
 constexpr int kKTileBytes = kKT * kHeadDim * 2;
+// Fourth word of a gfx9 buffer resource for raw (untyped) loads: 32-bit data
+// format, no swizzle, no index stride.
+constexpr int kBufferWord3 = 0x00020000;
 constexpr int kBufBytes = 2 * kKTileBytes;
 
 // LDS byte offset (within a buffer) of keys 32 h + 8 q .. +7 of dim d (V^T).
@@ -259,16 +262,45 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
     }
     st.vrow = true;
   };
+  // Full chunk tile: every key is the chunk's own and inside [klo, khi]. The
+  // tile's 64 rows of k_new / v_new start at a wave-uniform address and each
+  // lane's pieces sit at fixed byte offsets from it (rows of Hkv D 2 bytes), so
+  // the loads are buffer loads from a scalar resource with those offsets: no
+  // per-tile vector address arithmetic and no per-lane range checks.
+  const uint32_t row_bytes = (uint32_t)hkv * (kHeadDim * 2);
+  const bool chunk_buf = (uint64_t)hkv * (kHeadDim * 2) * kKT <= 0x7fffffffull;
+  uint32_t ch_koff[kStage], ch_voff[kStage];
+  {
+    const int r = lane & 15, ab = wave >> 2, c = 4 * (wave & 3) + (lane >> 4);
+#pragma unroll
+    for (int i = 0; i < kStage; ++i) {
+      ch_koff[i] = (uint32_t)(32 * i + 8 * (r >> 2) + 4 * ab + (r & 3)) * row_bytes + (uint32_t)c * 16u;
+      ch_voff[i] = (uint32_t)(8 * wave + 4 * i + (lane >> 4)) * row_bytes + (uint32_t)(lane & 15) * 16u;
+    }
+  }
+  auto load_tile_chunk_full = [&](int kt, Stage &st) __attribute__((always_inline)) {
+    const int64_t row0 = ((int64_t)(tok0 + kt - P) * hkv + g) * kHeadDim;
+    const __amdgpu_buffer_rsrc_t krs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.k_new + row0), 0, kKT * row_bytes, kBufferWord3);
+    const __amdgpu_buffer_rsrc_t vrs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(p.v_new + row0), 0, kKT * row_bytes, kBufferWord3);
+#pragma unroll
+    for (int i = 0; i < kStage; ++i) {
+      st.k[i] = __builtin_amdgcn_raw_buffer_load_b128(krs, (int)ch_koff[i], 0, 0);
+      st.v[i] = __builtin_amdgcn_raw_buffer_load_b128(vrs, (int)ch_voff[i], 0, 0);
+    }
+    st.vrow = true;
+  };
   // Interior tile: every key cached, in range and (PG >= 64) on one page whose
   // id was fetched ahead; the K tile is two 8 KiB K blocks and the V tile two
   // [D][32] blocks of 8 KiB, all contiguous: plain 16-byte loads, consecutive
   // threads at consecutive addresses.
   // The tile's two base addresses are wave-uniform (scalar registers) and each
-  // load adds a fixed 32-bit per-lane byte offset, so the loads take the
-  // scalar-base form with no per-tile vector address arithmetic.
+  // load adds a fixed 32-bit per-lane byte offset (buffer loads), so a tile's
+  // loads need no vector address arithmetic.
   // (The empty asm keeps the offsets opaque: the compiler would otherwise fold
-  // the constant 8 KiB step between a thread's two pieces into 64-bit vector
-  // address arithmetic.)
+  // the constant 8 KiB step between a thread's two pieces into arithmetic of
+  // its own.)
   uint32_t pg_koff[kStage] = {(uint32_t)tid * 16u, (uint32_t)(tid + kThreads) * 16u};
   uint32_t pg_voff[kStage] = {(uint32_t)(v_piece_dim(tid) * 32 + ((tid >> 4) & 3) * 8) * 2u,
                               (uint32_t)(32 * kHeadDim + v_piece_dim(tid) * 32 + ((tid >> 4) & 3) * 8) * 2u};
@@ -285,10 +317,15 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
                        (uint64_t)(((uint32_t)kt & (uint32_t)(pg - 1)) >> 5) * 8192u;
     const char *kbase = reinterpret_cast<const char *>(pv.k_pool) + o;
     const char *vbase = reinterpret_cast<const char *>(pv.v_pool) + o;
+    // buffer loads: the tile's 16 KiB from a scalar resource on its first
+    // byte plus this lane's fixed 32-bit offset, so a tile's four loads need
+    // no vector address arithmetic (offsets past the 16 KiB would read 0)
+    const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(kbase), 0, kKTileBytes, kBufferWord3);
+    const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(vbase), 0, kKTileBytes, kBufferWord3);
 #pragma unroll
     for (int i = 0; i < kStage; ++i) {
-      st.k[i] = ldg128_global(kbase + pg_koff[i]);
-      st.v[i] = ldg128_global(vbase + pg_voff[i]);
+      st.k[i] = __builtin_amdgcn_raw_buffer_load_b128(krs, (int)pg_koff[i], 0, 0);
+      st.v[i] = __builtin_amdgcn_raw_buffer_load_b128(vrs, (int)pg_voff[i], 0, 0);
     }
     st.vrow = false;
   };
@@ -394,6 +431,7 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   };
   auto fetch = [&](int kt, int page, Stage &st) __attribute__((always_inline)) {
     if (page >= 0 && interior(kt)) load_tile_page(kt, page, st);
+    else if (kt >= P && chunk_buf && kt >= klo && kt + kKT - 1 <= khi) load_tile_chunk_full(kt, st);
     else if (kt >= P) load_tile_chunk(kt, st);
     else load_tile(kt, page, st);
   };
@@ -422,7 +460,12 @@ __global__ __launch_bounds__(kThreads) void prefill_kernel(PrefillParams p) {
   auto mask_half = [&](int kt, int h, f32x4 (&sc)[2][kCG]) {
     // this lane's 8 keys are kt + 32h + 8q + e, e = 4 ab + i; allowed e form
     // the interval [lo_e, hi_e] of the column's visible keys
-    const int j0 = kt + 32 * h + 8 * q;
+    // kt laundered: the per-lane bounds below are then formed here, in the
+    // masked tiles only, not carried through the loop as vector induction
+    // variables that every tile would update
+    int ktl = kt;
+    asm volatile("" : "+s"(ktl));
+    const int j0 = ktl + 32 * h + 8 * q;
 #pragma unroll
     for (int cg = 0; cg < kCG; ++cg) {
       const int lo_e = max(max(clo[cg], klo) - j0, 0);
