@@ -63,6 +63,18 @@ def test_prefill_groups(gpu_lib, hq, hkv):
         assert_close(gpu, ref, f"prefill groups {kind} hq={hq} hkv={hkv}")
 
 
+@pytest.mark.parametrize("hq,hkv", [(32, 32), (64, 16)])
+def test_prefill_many_kv_heads(gpu_lib, hq, hkv):
+    """More KV heads than the configs' 8: chunk rows of Hkv * 256 bytes, read by
+    the full-chunk-tile buffer loads at per-lane row offsets, and page-heads of
+    Hkv * PG * 256 bytes for the interior tiles (PG 64); FULL, and SWA with a
+    window that takes the FULL kernel's masked path."""
+    print(f"[prefill-many-kv] hq={hq} hkv={hkv}", flush=True)
+    for kind, window in (("full", 0), ("swa", 1000)):
+        gpu, ref, _ = run_prefill(kind, window, 64, hq, hkv, [0, 130, 1100], [300, 200, 129], (308, hq, hkv))
+        assert_close(gpu, ref, f"prefill many KV heads {kind} hq={hq} hkv={hkv}")
+
+
 def test_prefill_long_chunk_over_prefix(gpu_lib):
     """A 2048-token chunk over a 1000-token prefix, FULL and SWA (wraps the ring)."""
     for kind, window in (("full", 0), ("swa", 128)):
