@@ -55,14 +55,14 @@ FLUSH_BYTES = 1 << 30  # a write this large evicts the 256 MB memory-side cache
 # measured again.
 MEASURED_TRAFFIC = {
     "decode_full_stack70": {"sources": ["decode.hip", "hswa_common.h", "hswa_launch.h"],
-                            "sha256": "13d68500ed422956e601499e5a6acd76855b074147037a96c9615d0e73ffd3a6",
-                            "fetch_bytes": 8610120847, "write_bytes": 5120045},
+                            "sha256": "9f79f244d635ed49e89f86766b226dfc1713af51a94af90ffecde4a27184a1c1",
+                            "fetch_bytes": 8609292305, "write_bytes": 5574508},
     "prefill_full": {"sources": ["prefill.hip", "hswa_common.h", "hswa_launch.h"],
-                     "sha256": "b5d6ebe3c313260bcd14426b0f9593b3a2ba6b4e399903c7cdc871b5705d7b4f",
-                     "fetch_bytes": 452820666, "write_bytes": 141551869},
+                     "sha256": "09c415c25425ca9092c56d08c06cfb6cdf7ea89fd23249c800f47ff74d31818f",
+                     "fetch_bytes": 453240070, "write_bytes": 141568870},
     "prefill_swa": {"sources": ["prefill_run.hip", "hswa_common.h", "hswa_launch.h"],
-                    "sha256": "0ec3136d4a24e36565e979acac7ee62b79bdfd47b5617eeba99ce8c6b5af775c",
-                    "fetch_bytes": 184793088, "write_bytes": 149660365},
+                    "sha256": "1ab52ecfb56b32547d74b3a6bf166c7dc311a3e9828d48afb8205e14c9a02211",
+                    "fetch_bytes": 184794072, "write_bytes": 149292872},
 }
 
 

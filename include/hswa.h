@@ -249,8 +249,10 @@ hswa_status hswa_decode(hswa_layer layer, const hswa_shape *shape, const hswa_ca
  * out[b] as hswa_decode with the same context_lens would after that append.
  * Sequences with c_b < 1 store nothing and get a zero row. SWA layers, and FULL
  * layers short enough for one pass, do both in one kernel whose new key comes
- * from k_new / v_new (results equal the two calls' up to rounding order); other
- * FULL layers run the append kernel, then the decode kernels.
+ * from k_new / v_new (results equal the two calls' up to rounding order); so
+ * do the split-KV decode kernels of longer FULL layers when page_size >= 32
+ * (the log-sum-exp merge still follows); FULL layers with page_size 16 run the
+ * append kernel, then the decode kernels.
  * k_new, v_new: device bf16 [ns][Hkv][D]; the other arguments as hswa_decode.
  * The call must not overlap another call writing the same layer's pools. */
 hswa_status hswa_decode_append(hswa_layer layer, const hswa_shape *shape, const hswa_cache *cache,

@@ -287,6 +287,11 @@ hswa_status decode_impl(hswa_layer layer, const hswa_shape *shape, const hswa_ca
     p.k_new = static_cast<const uint16_t *>(k_new);
     p.v_new = static_cast<const uint16_t *>(v_new);
     if (hswa::decode_append_fused(p)) return finish_launch(hswa::launch_decode_append(p, s), s);
+    if (p.max_splits > 1 && p.nq == 1 && pv.pg_shift >= 5) {
+      // FULL split path: the split decode stores the token itself
+      p.split_append = 1;
+      return finish_launch(hswa::launch_decode(p, s), s);
+    }
     hswa::AppendParams a{};
     a.pool = pv;
     a.k_new = p.k_new;

@@ -435,6 +435,51 @@ void decode_kernel(DecodeParams p) {
         };
         // this wave's chunks: c0, c0 + kCoop, ...
         const int nw = nchunks > c0 ? (nchunks - c0 + kCoop<kSplit> - 1) / kCoop<kSplit> : 0;
+        // Fused append (split spans, one query per sequence): the piece that
+        // holds the segment's last chunk holds the step's token at `pos`. Its
+        // key is not in the pool yet: this lane's pieces of it come from
+        // k_new / v_new and replace what the chunk's loads read for that key,
+        // and the first head group's wave stores the row in its slot.
+        const bool app = kSplit && p.split_append && nw > 0 && c_hi == nch;
+        u32x4 kapp[4];
+        uint32_t vapp[8];
+        int app_page = -1;  // the token's page (-1: invalid, nothing stored)
+        if (app) {
+          const int64_t kvrow = ((int64_t)b * hkv + g) * kHeadDim;
+#pragma unroll
+          for (int t = 0; t < 4; ++t) kapp[t] = ldg128(p.k_new + kvrow + 32 * t + 8 * q);
+#pragma unroll
+          for (int dt = 0; dt < 8; ++dt) vapp[dt] = p.v_new[kvrow + 16 * dt + r];
+          const int lp = pos >> shift;
+          if (lp < pv.stride) {
+            const int64_t v = pv.table[(int64_t)b * pv.stride + lp];
+            app_page = v >= 0 && v < pv.num_pages ? (int)v : -1;
+          }
+        }
+        // the new key kc = pos % 32 of the last chunk: K rows of MFMA row
+        // 4 (kc / 8) + kc % 4 in half (kc / 4) % 2 (dims 32 t + 8 q .. +7 in
+        // lane r + 16 q); V pieces of lanes q = kc / 8, element kc % 8
+        auto patch = [&](Chunk &ch) {
+          const int kc = pos & (kChunk - 1);
+          const bool kl = r == 4 * (kc >> 3) + (kc & 3);
+          const bool hb = (kc >> 2) & 1;
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            ch.ka[t] = kl && !hb ? kapp[t] : ch.ka[t];
+            ch.kb[t] = kl && hb ? kapp[t] : ch.kb[t];
+          }
+          const bool vl = q == (kc >> 3);
+          const int e = kc & 7, sh = 16 * (e & 1);
+          const uint32_t msk = 0xFFFFu << sh;
+#pragma unroll
+          for (int dt = 0; dt < 8; ++dt) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const uint32_t w = (ch.v[dt][j] & ~msk) | (vapp[dt] << sh);
+              ch.v[dt][j] = vl && j == (e >> 1) ? w : ch.v[dt][j];
+            }
+          }
+        };
         if (kSplit && nw > 0) {
           // Split spans (long streams of chunks): one wave per SIMD, two whole
           // chunks in flight while a third is computed. Chunk k is computed
@@ -450,14 +495,31 @@ void decode_kernel(DecodeParams p) {
           };
           issue_both(0, ca);
           issue_both(min(1, nw - 1), cb);
+          if (app && hc == 0 && app_page >= 0) {
+            // the append, early so that its stores are done long before the
+            // kernel ends: the token's K row (lanes r = 0 hold dims
+            // 32 t + 8 q) and V column (lanes q = 0 hold dims 16 dt + r)
+            const int o = pos & (pg - 1);
+            if (r == 0) {
+#pragma unroll
+              for (int t = 0; t < 4; ++t)
+                stg128(pv.k_pool + k_offset(pv, app_page, hkv, g, o, 32 * t + 8 * q), kapp[t]);
+            }
+            if (q == 0) {
+#pragma unroll
+              for (int dt = 0; dt < 8; ++dt) pv.v_pool[v_offset(pv, app_page, hkv, g, o, 16 * dt + r)] = (uint16_t)vapp[dt];
+            }
+          }
           u32x4 pf[kCGd];
           int k = 0;
           for (; k + 2 <= nw; k += 2) {
+            if (app && k == nw - 1) patch(ca);
             scores(ca, pf);
             pv_update(ca, pf);
             __builtin_amdgcn_sched_barrier(0);
             issue_both(min(k + 2, nw - 1), ca);
             __builtin_amdgcn_sched_barrier(0);
+            if (app && k + 1 == nw - 1) patch(cb);
             scores(cb, pf);
             pv_update(cb, pf);
             __builtin_amdgcn_sched_barrier(0);
@@ -465,6 +527,7 @@ void decode_kernel(DecodeParams p) {
             __builtin_amdgcn_sched_barrier(0);
           }
           if (k < nw) {
+            if (app) patch(ca);
             scores(ca, pf);
             pv_update(ca, pf);
           }

@@ -61,6 +61,9 @@ struct DecodeParams {
   float scale_log2;       // scale * log2(e)
   const uint16_t *k_new;  // decode step: the new token's K / V rows [ns][Hkv][D]
   const uint16_t *v_new;
+  // FULL split decode of one new token per sequence, PG >= 32: the kernel also
+  // stores the token (k_new / v_new) in its slot and takes its key from them
+  int32_t split_append;
 };
 
 struct PrefillParams {

@@ -7,9 +7,10 @@ layer B runs hswa_kv_append of that token, then hswa_decode. The checks:
   * A's pools equal B's bit for bit (NaN-filled unused slots included), so
     the fused store is exactly the append;
   * A's output matches B's within the same tolerance.
-The cases span both kernels behind the call (the fused one for SWA windows
-and short FULL contexts at PG >= 32; the append kernel plus the decode
-kernels for PG 16, windows over 8 chunks and split FULL contexts), windows
+The cases span the kernels behind the call (the fused one for SWA windows
+and short FULL contexts at PG >= 32; the split decode storing the token for
+longer FULL contexts at PG >= 32; the append kernel plus the decode kernels
+for PG 16 and windows over 8 chunks), windows
 around chunk and page sizes, GQA groups 1 to 32, empty sequences and an
 invalid page under the new token."""
 
@@ -112,10 +113,35 @@ def test_decode_append_groups(gpu_lib, hq, hkv):
 @pytest.mark.parametrize("pg", [32, 64])
 def test_decode_append_full(gpu_lib, pg):
     """FULL: contexts of at most 256 keys take the fused kernel; a longer
-    batch the split decode after the append kernel."""
+    batch the split decode, which stores the token itself."""
     print(f"[decode-append full] pg={pg}", flush=True)
     check(run_step("full", 0, pg, 64, 8, [1, 2, 31, 32, 33, 100, 255, 256], (302, pg)), f"full short PG={pg}")
     check(run_step("full", 0, pg, 64, 8, [1, 257, 1000, 5000, 0], (303, pg)), f"full split PG={pg}")
+
+
+@pytest.mark.parametrize("hq,hkv", [(32, 1), (64, 1), (16, 16)])
+def test_decode_append_full_split_groups(gpu_lib, hq, hkv):
+    """FULL split path, where the split decode stores the token itself: GQA
+    groups of 32 and 64 (two column groups per wave; at 64 two head-group items
+    per KV head, of which only the first stores) and 16 KV heads of group 1."""
+    print(f"[decode-append full split] hq={hq} hkv={hkv}", flush=True)
+    lens = [1, 300, 2000, 5000, 0, 4097]
+    shape = hswa.Shape(hq, hkv, D, 64)
+    assert max(lens) > hswa.decode_split_len(shape, len(lens), max(lens))  # the split path
+    check(run_step("full", 0, 64, hq, hkv, lens, (306, hq, hkv)), f"full split hq={hq} hkv={hkv}")
+
+
+def test_decode_append_full_split_invalid_page(gpu_lib):
+    """FULL split path with the token's page entry invalid (-1, or past the
+    pool): nothing is stored and the key is left out, as the two calls do."""
+    print("[decode-append full split invalid page]", flush=True)
+    lens, pg = [5000, 4097, 300], 64
+
+    def edit(table):
+        table[0, 4999 // pg] = -1
+        table[1, 4096 // pg] = 1 << 30
+
+    check(run_step("full", 0, pg, 64, 8, lens, (307,), table_edit=edit), "full split invalid page", oracle=False)
 
 
 def test_decode_append_swa_paged(gpu_lib):
