@@ -55,8 +55,8 @@ FLUSH_BYTES = 1 << 30  # a write this large evicts the 256 MB memory-side cache
 # measured again.
 MEASURED_TRAFFIC = {
     "decode_full_stack70": {"sources": ["decode.hip", "hswa_common.h", "hswa_launch.h"],
-                            "sha256": "9f79f244d635ed49e89f86766b226dfc1713af51a94af90ffecde4a27184a1c1",
-                            "fetch_bytes": 8609292305, "write_bytes": 5574508},
+                            "sha256": "a816581b63dc9b938f32c3a6c2523b1b073f47161d1870bdb747704808bd0fc3",
+                            "fetch_bytes": 8609499338, "write_bytes": 5574682},
     "prefill_full": {"sources": ["prefill.hip", "hswa_common.h", "hswa_launch.h"],
                      "sha256": "09c415c25425ca9092c56d08c06cfb6cdf7ea89fd23249c800f47ff74d31818f",
                      "fetch_bytes": 453240070, "write_bytes": 141568870},

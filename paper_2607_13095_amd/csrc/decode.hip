@@ -512,8 +512,8 @@ void decode_kernel(DecodeParams p) {
           }
           u32x4 pf[kCGd];
           int k = 0;
+          // the last chunk (index nw - 1) is the loop's second one or the tail's
           for (; k + 2 <= nw; k += 2) {
-            if (app && k == nw - 1) patch(ca);
             scores(ca, pf);
             pv_update(ca, pf);
             __builtin_amdgcn_sched_barrier(0);
