@@ -55,7 +55,7 @@ FLUSH_BYTES = 1 << 30  # a write this large evicts the 256 MB memory-side cache
 # measured again.
 MEASURED_TRAFFIC = {
     "decode_full_stack70": {"sources": ["decode.hip", "hswa_common.h", "hswa_launch.h"],
-                            "sha256": "a816581b63dc9b938f32c3a6c2523b1b073f47161d1870bdb747704808bd0fc3",
+                            "sha256": "33e861862964a2599c57b8f8b62732bb38b9230475ce145bad52e97f5f5aaef7",
                             "fetch_bytes": 8609499338, "write_bytes": 5574682},
     "prefill_full": {"sources": ["prefill.hip", "hswa_common.h", "hswa_launch.h"],
                      "sha256": "09c415c25425ca9092c56d08c06cfb6cdf7ea89fd23249c800f47ff74d31818f",

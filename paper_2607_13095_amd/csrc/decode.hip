@@ -29,6 +29,10 @@
 // QK^T runs. A segment cut by span boundaries
 // gets fp32 (o, log2 sum-exp) partials that a second kernel merges; a segment
 // inside one span, and a whole-range item, is written as bf16 directly.
+// In a decode step with its append ("KVCache Dual-Pool Design": the step's
+// token goes to its slot), the split spans of one-page chunks also store the
+// token: the wave holding a segment's last chunk takes the token's key from
+// the input rows and writes them to the slot.
 #include <atomic>
 #include <cfloat>
 
