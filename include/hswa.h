@@ -79,7 +79,7 @@
  *   hswa_kv_append of the chunk. For SWA this order is required: a chunk
  *   longer than the ring overwrites prefix keys that its first queries need.
  * Supported shapes: head_dim == 128; Hq % Hkv == 0 and 128 % (Hq/Hkv) == 0;
- *   page_size a power of two in [16, 256]; SWA window >= 1.
+ *   Hkv <= 4096; page_size a power of two in [16, 256]; SWA window >= 1.
  *   Anything else returns HSWA_ERR_UNSUPPORTED or HSWA_ERR_INVALID_ARG.
  */
 #ifndef HSWA_H

@@ -31,6 +31,8 @@ int log2_exact(int32_t x) {
   return s;
 }
 
+constexpr int32_t kMaxKvHeads = 4096;
+
 // Shape checks shared by every device call.
 hswa_status check_shape(const hswa_shape *sh) {
   if (!sh) return HSWA_ERR_INVALID_ARG;
@@ -39,6 +41,9 @@ hswa_status check_shape(const hswa_shape *sh) {
   if (sh->num_q_heads % sh->num_kv_heads != 0) return HSWA_ERR_INVALID_ARG;
   if (!(sh->scale > 0.f) || !std::isfinite(sh->scale)) return HSWA_ERR_INVALID_ARG;
   if (sh->head_dim != hswa::kHeadDim) return HSWA_ERR_UNSUPPORTED;
+  // a page-head of every KV head (Hkv * PG * D * 2 bytes) stays under 2^32,
+  // which the kernels' 32-bit page strides assume
+  if (sh->num_kv_heads > kMaxKvHeads) return HSWA_ERR_UNSUPPORTED;
   const int group = sh->num_q_heads / sh->num_kv_heads;
   if (128 % group != 0) return HSWA_ERR_UNSUPPORTED;
   const int s = log2_exact(sh->page_size);

@@ -103,6 +103,7 @@ FULL, SWA128 = hswa._Layer(0, 0), hswa._Layer(1, 128)
     (_shape(pg=48), -2), (_shape(pg=8), -2), (_shape(pg=512), -2),
     (_shape(scale=0.0), -1), (_shape(scale=float("nan")), -1),
     (_shape(hq=0), -1),
+    (_shape(hq=8192, hkv=8192), -2),                   # more than 4096 KV heads
 ])
 def test_decode_shape_validation(shape, code):
     assert _decode(FULL, shape, _cache()) == code
